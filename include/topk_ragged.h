@@ -1,0 +1,160 @@
+/*
+ * topk_ragged -- exact Top-K over ragged FP32 score rows on AMD MI355X (gfx950).
+ *
+ * Implements the sample-guided exact selection of "Sample-Guided Exact Top-K
+ * Selection for Long-Context Sparse Attention" (arXiv 2609.08450):
+ *   Phase 1  a fixed-stride, row-phased view proposes a coarse boundary
+ *            (Section 4.2, eq:method:view .. eq:method:primary-threshold);
+ *   Phase 2  one complete-row pass certifies it and compacts the admitted
+ *            candidates (Section 4.3, eq:method:candidate-set, Lemma
+ *            lem:method:containment), with a nested secondary boundary and
+ *            exact coarse recovery for underfilled proposals
+ *            (eq:method:rescue-band, eq:method:exact-init);
+ *   Phase 3  exact radix refinement over the surviving frontier
+ *            (Section 4.4, eq:method:refine-prefix .. refine-recurrence),
+ * behind a ragged-row dispatcher: rows with L <= K are written directly,
+ * short rows run on one workgroup, long rows are split across several
+ * workgroups whose admitted candidates are merged by the last one to finish
+ * (Section 4.5, eq:method:split-local, eq:method:split-reduce).
+ *
+ * Semantics (Section 2.1 operator contract, with the choices the paper leaves
+ * open fixed as follows):
+ *   - order is that of the order-preserving uint32 transform of the FP32 bits:
+ *     -inf < ... < -0.0 < +0.0 < ... < +inf, subnormals ordered; no NaN input;
+ *   - ties at rank K go to the lowest index;
+ *   - row r with L_r = max(0, row_lengths[r]) <= K returns indices 0..L_r-1 in
+ *     order, then -1 with value -inf;
+ *   - for L_r > K the K returned (index, value) pairs are in no particular
+ *     order.
+ *
+ * All entry points are host functions returning a status code synchronously.
+ * Device pointers are caller-owned; the library never allocates, never
+ * synchronises (except topk_ragged_read_stats) and enqueues only on `stream`,
+ * so topk_ragged can be captured in a HIP graph.  `stream` is a hipStream_t
+ * passed as void* (NULL = the default stream).
+ */
+#ifndef TOPK_RAGGED_H
+#define TOPK_RAGGED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define TOPK_OK 0
+#define TOPK_EINVAL (-1)       /* bad scalar argument or null pointer */
+#define TOPK_EUNSUPPORTED (-2) /* current device is not gfx950 */
+#define TOPK_ELAUNCH (-3)      /* a HIP call failed (see hipGetLastError) */
+#define TOPK_EWORKSPACE (-4)   /* workspace too small for the plan */
+
+/* Largest supported K.  Results are exact for every K up to this value; the
+ * sampled pipeline is tuned for K around 2048 (K~ = 1.5 K candidates must fit
+ * the on-chip frontier of TOPK_FRONTIER_CAP entries). */
+#define TOPK_K_MAX 16384
+/* Frontier capacity of one workgroup, in (index, key) pairs. */
+#define TOPK_FRONTIER_CAP 8192
+/* Words per row written by topk_ragged_ex when row_trace is not NULL. */
+#define TOPK_TRACE_WORDS 8
+
+/* Route codes (trace word 0, and the stats counters). */
+#define TOPK_ROUTE_DIRECT 0          /* L <= K */
+#define TOPK_ROUTE_PRIMARY 1         /* C(tau0) >= K, certified proposal */
+#define TOPK_ROUTE_BAND 2            /* C(tau0) < K <= C(tau1), band extension */
+#define TOPK_ROUTE_EXACT_UNSAMPLED 3 /* view unusable or row below sampling floor */
+#define TOPK_ROUTE_EXACT_UNDERFILL 4 /* C(tau1) < K: exact coarse recovery */
+#define TOPK_ROUTE_EXACT_OVERFLOW 5  /* admitted tail larger than the frontier */
+#define TOPK_ROUTE_REREAD_FLAG 16    /* or-ed in: exact boundary bin larger than
+                                        the frontier, resolved by re-reading */
+
+/* Policy of the sampled pipeline (Section 4.2 constants).  The defaults are
+ * s = 128, K~ = 1.5 K, K~1 = 1.75 K (the configuration the paper evaluates),
+ * sampling floor 4 K elements, frontier capacity TOPK_FRONTIER_CAP. */
+typedef struct topk_ragged_policy {
+    int32_t s_log2;     /* view stride s = 2^s_log2, 0 <= s_log2 <= 12 */
+    int32_t rho_num;    /* K~  = ceil(rho_num  K / rho_den)  (as sample rank) */
+    int32_t rho_den;
+    int32_t rho1_num;   /* K~1 = ceil(rho1_num K / rho1_den) (nested target) */
+    int32_t rho1_den;
+    int32_t l_samp_min; /* rows shorter than this take the exact route; a
+                           negative value -m means m * K */
+    int32_t cap;        /* frontier capacity, 1 <= cap <= TOPK_FRONTIER_CAP */
+} topk_ragged_policy;
+
+/* Route counters accumulated in the workspace (one increment per row with
+ * L > K or L <= K), and error/diagnostic counts. */
+typedef struct topk_ragged_stats {
+    uint64_t route[6];     /* indexed by TOPK_ROUTE_* (flag stripped) */
+    uint64_t reread;       /* rows that took the re-read fallback */
+    uint64_t wait_fallback;/* split segments that recomputed the view locally */
+    uint64_t errors;       /* calls rejected on the device (bad workspace) */
+} topk_ragged_stats;
+
+/* Fills *out with the default policy.  Returns TOPK_OK. */
+int topk_ragged_default_policy(topk_ragged_policy *out);
+
+/* Bytes of workspace needed for calls with n_rows <= max_rows and this K on
+ * the current device.  Independent of row lengths: per-row state is kept only
+ * for rows split across workgroups, and at most 4 x (compute units) rows are
+ * ever split.  Returns 0 for invalid arguments. */
+size_t topk_ragged_workspace_size(int32_t max_rows, int32_t K);
+
+/* One-time initialisation of a workspace of `bytes` bytes (enqueued on
+ * `stream` with kernels only, no memset nodes).  Must run before the first
+ * topk_ragged call on that workspace.  Kernels leave the workspace ready for
+ * the next call, so graph replays need no re-initialisation. */
+int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, int32_t K,
+                               void *stream);
+
+/* Exact Top-K of every row.
+ *   scores       device, FP32; row r is scores[row_offsets[r] ..
+ *                row_offsets[r] + row_lengths[r]).  Rows may be packed
+ *                back-to-back or padded to a pitch (row_offsets[r] = r*pitch);
+ *                any 4-byte alignment is accepted.  Must be free of NaN.
+ *   row_offsets  device, int64 [n_rows], element offsets (>= 0).
+ *   row_lengths  device, int32 [n_rows], valid lengths (negative = 0).
+ *   n_rows       >= 0; 0 is a no-op.
+ *   K            1 <= K <= TOPK_K_MAX.
+ *   out_idx      device, int32 [n_rows x K], row-relative indices.
+ *   out_val      device, FP32 [n_rows x K], bit-exact copies of the scores.
+ *   workspace    device, initialised by topk_ragged_workspace_init with
+ *                max_rows >= n_rows; not shared by concurrent calls.
+ * Row lengths and offsets stay on the device; the launch geometry depends
+ * only on (n_rows, K, device).  If the workspace is invalid for n_rows the
+ * kernel writes -1 / -inf to every output and counts an error in the stats.
+ * Returns TOPK_OK or an error code; nothing is enqueued on error. */
+int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
+                int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
+                void *stream);
+
+/* topk_ragged with an explicit policy (NULL = default) and an optional
+ * per-row trace (device, int32 [n_rows x TOPK_TRACE_WORDS], NULL = none):
+ *   [0] route (TOPK_ROUTE_*, TOPK_ROUTE_REREAD_FLAG or-ed in), [1] view size
+ *   |V| (-1 if L <= K), [2] tau0, [3] tau1 (-1 if not sampled), [4] C(tau0),
+ *   [5] C(tau1) (-1 if not evaluated), [6] tau_star (-1 unless exact coarse
+ *   recovery ran), [7] |Q0| entering refinement (-1 if L <= K). */
+int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
+                   int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
+                   const topk_ragged_policy *policy, int32_t *row_trace, void *stream);
+
+/* Copies the workspace's accumulated counters to *out (host) and resets them.
+ * Synchronises `stream`.  For diagnostics outside timed regions. */
+int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream);
+
+/* Building-block probes for tests (device pointers):
+ * coarse bins c(x) of n values (eq:method:coarse-map) into uint16 out_c, and
+ * the inclusive ascending-key endpoint of each of the 2048 coarse bins into
+ * out_cut (0xFFFFFFFF when no value falls in bins <= tau). */
+int topk_ragged_debug_coarse(const float *x, int64_t n, uint16_t *out_c, void *stream);
+int topk_ragged_debug_cutoffs(uint32_t *out_cut, void *stream);
+
+/* Human-readable text for a status code. */
+const char *topk_ragged_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TOPK_RAGGED_H */

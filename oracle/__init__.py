@@ -61,7 +61,7 @@ def lib():
         P = ctypes.c_void_p
         L.oracle_topk_ragged.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, ctypes.c_int]
         L.oracle_topk_ragged.restype = ctypes.c_int
-        L.oracle_route_model.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32,
+        L.oracle_route_model.argtypes = [P, P, P, P, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.POINTER(Policy), P, P, P, ctypes.c_int]
         L.oracle_route_model.restype = ctypes.c_int
         L.oracle_asc32.argtypes = [ctypes.c_uint32]
@@ -122,15 +122,22 @@ def default_policy(**kw) -> Policy:
 
 
 def route_model(scores, row_offsets, row_lengths, K: int, policy: Policy | None = None,
-                n_threads: int = 0):
-    """Step-by-step pipeline model.  Returns (idx, val, trace [n, 8] int32)."""
+                n_threads: int = 0, row_ids=None):
+    """Step-by-step pipeline model.  Returns (idx, val, trace [n, 8] int32).
+    row_ids: original row numbers (they select the view phase) when the rows
+    are a subset of a larger call."""
     scores, offs, lens = _rows(scores, row_offsets, row_lengths)
     policy = policy or default_policy()
     n = len(lens)
+    ids = None
+    if row_ids is not None:
+        ids = np.ascontiguousarray(row_ids, dtype=np.int32)
+        assert ids.shape == lens.shape
     oi = np.empty((n, K), np.int32)
     ov = np.empty((n, K), np.float32)
     tr = np.empty((n, TRACE_WORDS), np.int32)
-    rc = lib().oracle_route_model(_ptr(scores), _ptr(offs), _ptr(lens), n, K,
+    rc = lib().oracle_route_model(_ptr(scores), _ptr(offs), _ptr(lens),
+                                  _ptr(ids) if ids is not None else None, n, K,
                                   ctypes.byref(policy), _ptr(oi), _ptr(ov), _ptr(tr), n_threads)
     if rc != 0:
         raise RuntimeError(f"oracle_route_model failed: {rc}")

@@ -318,7 +318,10 @@ static void refine(const float *x, uint32_t *Q, int64_t nQ, int64_t k,
     free(h);
 }
 
-/* Route model of the sampled pipeline for every row.  Writes the selection to
+/* Route model of the sampled pipeline for every row.  row_ids (may be NULL)
+ * gives the row number that selects each row's view phase, so a subset of a
+ * larger call can be modelled; NULL means row r uses phase a_r of r.
+ * Writes the selection to
  * out_idx / out_val (any order within a row for L > K; direct layout for
  * L <= K) and, when trace != NULL, 8 int32 per row:
  *   [0] route (ROUTE_*; ROUTE_REREAD_FLAG or-ed in when an exact boundary bin
@@ -327,8 +330,8 @@ static void refine(const float *x, uint32_t *Q, int64_t nQ, int64_t k,
  *   [6] tau_star (-1 unless exact recovery ran), [7] |Q0| entering refinement
  *   (-1 for L <= K). */
 int oracle_route_model(const float *scores, const int64_t *row_offsets,
-                       const int32_t *row_lengths, int32_t n_rows, int32_t K,
-                       const oracle_policy *pol, int32_t *out_idx, float *out_val,
+                       const int32_t *row_lengths, const int32_t *row_ids, int32_t n_rows,
+                       int32_t K, const oracle_policy *pol, int32_t *out_idx, float *out_val,
                        int32_t *trace, int n_threads) {
     if (n_rows < 0 || K < 1 || !pol || pol->s < 1 || (pol->s & (pol->s - 1)))
         return -1;
@@ -370,7 +373,7 @@ int oracle_route_model(const float *scores, const int64_t *row_offsets,
             c[i] = oracle_coarse(x[i]);
 
         /* Phase 1: row-phased view and its coarse histogram. */
-        int32_t a = oracle_phase(r, s);
+        int32_t a = oracle_phase(row_ids ? row_ids[r] : r, s);
         int64_t nv = (a < L) ? ceil_div64(L - a, s) : 0;
         tr[1] = (int32_t)nv;
         int route;

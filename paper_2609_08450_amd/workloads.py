@@ -216,3 +216,34 @@ CONFIGS = {
 
 def make(config: int, **kw) -> Workload:
     return CONFIGS[config](**kw)
+
+
+def chunked_prefill_device(device, seed: int = BASE_SEED + 3, n_rows: int = 4096,
+                           context: int = 131072, dim: int = 64, heads: int = 8, K: int = 2048):
+    """The chunked-prefill block with the indexer product computed on `device`
+    (torch, FP32): the same seeded queries, keys and head weights as
+    `chunked_prefill`, much faster to build at full size.  Returns
+    (scores [n_rows * context] device tensor, row_offsets, row_lengths) with
+    numpy offsets/lengths; the score bits may differ from the host build."""
+    import torch
+
+    ss = np.random.SeedSequence(seed)
+    g = np.random.Generator(np.random.PCG64(ss))
+    keys = torch.from_numpy(g.standard_normal((context, dim), dtype=np.float32)).to(device)
+    w = g.random(heads, dtype=np.float32)
+    q = torch.from_numpy(g.standard_normal((n_rows, heads, dim), dtype=np.float32)).to(device)
+    scale = 1.0 / math.sqrt(dim)
+    out = torch.empty((n_rows, context), dtype=torch.float32, device=device)
+    kt = keys.t().contiguous()
+    chunk = 256
+    for r0 in range(0, n_rows, chunk):
+        r1 = min(n_rows, r0 + chunk)
+        acc = torch.zeros((r1 - r0, context), dtype=torch.float32, device=device)
+        for h in range(heads):
+            d = torch.mm(q[r0:r1, h, :].contiguous(), kt)
+            d.mul_(scale).clamp_(min=0).mul_(float(w[h]))
+            acc.add_(d)
+        out[r0:r1] = acc
+    lens = (context - n_rows + 1 + np.arange(n_rows)).astype(np.int32)
+    offs = np.arange(n_rows, dtype=np.int64) * context
+    return out.reshape(-1), offs, lens

@@ -1,0 +1,308 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle.
+
+Final selections are compared per row as (index, value-bits) sets with the
+plain-definition oracle (bit-exact); per-row route traces are compared with
+the oracle's step-by-step model (integer-exact).  Every case prints its name
+before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_08450_amd import workloads as W
+from tests.gpu_util import assert_same_selection, device_arrays, oracle_policy_of, run_hip
+from tests.invariants import check_row
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def topk():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_08450_amd import topk as T
+
+    T.lib()
+    return T
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def parity(topk, wl, policy=None, trace=True, where=""):
+    import torch
+
+    say(where or wl.name, "rows", wl.n_rows, "sum L", wl.total_len, "K", wl.K)
+    s, o, l = device_arrays(wl)
+    pol = policy or topk.default_policy()
+    gi, gv, gt, st = run_hip(s, o, l, wl.K, pol, trace)
+    oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, wl.K)
+    assert_same_selection(gi, gv, oi, ov, where=where or wl.name)
+    if trace:
+        _, _, mt = oracle.route_model(wl.scores, wl.row_offsets, wl.row_lengths, wl.K,
+                                      oracle_policy_of(pol, wl.K))
+        bad = np.nonzero(np.any(gt != mt, axis=1))[0]
+        assert bad.size == 0, (f"{where}: trace differs on {bad.size} rows, first row {bad[0]}: "
+                               f"gpu {gt[bad[0]].tolist()} oracle {mt[bad[0]].tolist()}")
+    assert st["errors"] == 0
+    del s, o, l
+    torch.cuda.synchronize()
+    return gt, st
+
+
+# ------------------------------------------------------- building blocks --
+
+def test_cutoffs_match_oracle(topk):
+    import torch
+
+    say("cutoffs")
+    out = torch.zeros(2048, dtype=torch.int32, device="cuda")
+    topk.debug_cutoffs(out)
+    got = out.cpu().numpy().view(np.uint32)
+    assert np.array_equal(got, oracle.cutoffs())
+
+
+def test_coarse_map_matches_oracle(topk):
+    import torch
+
+    say("coarse map")
+    top = np.arange(0, 1 << 19, dtype=np.uint32) << 13
+    low = np.array([0, 1, 0x0FFF, 0x1000, 0x1001, 0x1FFF], np.uint32)
+    pats = (top[:, None] | low[None, :]).ravel()
+    rng = np.random.default_rng(5)
+    pats = np.concatenate([pats, rng.integers(0, 1 << 32, 4_000_000, dtype=np.uint64).astype(np.uint32)])
+    x = pats.view(np.float32)
+    x = x[~np.isnan(x)]
+    xd = torch.from_numpy(x).cuda()
+    out = torch.empty(x.size, dtype=torch.int16, device="cuda")
+    topk.debug_coarse(xd, out)
+    got = out.cpu().numpy().view(np.uint16).astype(np.uint32)
+    want = oracle.coarse(x)
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, [(hex(int(x[i].view(np.uint32))), int(got[i]), int(want[i])) for i in bad[:5]]
+
+
+# ---------------------------------------------------------- workloads ----
+
+@pytest.mark.parametrize("cfg", [1, 2, 4, 5])
+def test_parity_config(topk, cfg):
+    wl = W.make(cfg)
+    gt, st = parity(topk, wl, where=f"config {cfg} ({wl.name})")
+    say("routes", st)
+
+
+def test_parity_adversarial_recovery(topk):
+    wl = W.adversarial_recovery()
+    gt, st = parity(topk, wl)
+    assert st["exact_underfill"] > 0 and st["band"] + st["exact_underfill"] > 0
+
+
+def test_parity_chunked_prefill_sampled_rows(topk):
+    """Full 4096 x 131072 causal block on the GPU; 64 rows checked against the
+    oracle (first, last and seeded random rows), with traces."""
+    import torch
+
+    say("chunked prefill 4096 rows (device-built scores)")
+    s, offs, lens = W.chunked_prefill_device("cuda")
+    n, K = lens.size, 2048
+    o = torch.from_numpy(offs).cuda()
+    l = torch.from_numpy(lens).cuda()
+    gi, gv, gt, st = run_hip(s, o, l, K, topk.default_policy(), True)
+    rng = np.random.default_rng(7)
+    rows = np.unique(np.concatenate([np.arange(8), np.arange(n - 8, n), rng.choice(n, 48, replace=False)]))
+    host = s.view(n, -1).cpu().numpy()
+    sub = W.Workload("prefill[rows]", np.concatenate([host[r, :lens[r]] for r in rows]),
+                     np.concatenate([[0], np.cumsum(lens[rows][:-1])]).astype(np.int64),
+                     lens[rows].astype(np.int32), K, "")
+    oi, ov = oracle.topk_ragged(sub.scores, sub.row_offsets, sub.row_lengths, K)
+    assert_same_selection(gi[rows], gv[rows], oi, ov, rows=rows, where="chunked prefill")
+    _, _, mt = oracle.route_model(sub.scores, sub.row_offsets, sub.row_lengths, K,
+                                  oracle_policy_of(topk.default_policy(), K), row_ids=rows)
+    assert np.array_equal(gt[rows], mt)
+    assert st["errors"] == 0 and st["direct"] == 0
+    say("routes", st)
+
+
+# -------------------------------------------------------- forced routes --
+
+def _mixed(K=2048):
+    rng = np.random.default_rng(11)
+    rows = []
+    for L in (K - 1, K, K + 1, 5000, 9000, 30000, 70000, 140000, 300000):
+        x = rng.standard_normal(L).astype(np.float32)
+        rows.append(x)
+        rows.append(np.round(x * 3).astype(np.float32))          # heavy ties
+    rows.append(np.full(20000, 0.25, np.float32))                # all equal, > cap
+    rows.append(np.where(rng.random(50000) < 0.5, -np.inf, 1.0).astype(np.float32))
+    buf = np.concatenate(rows)
+    lens = np.array([r.size for r in rows], np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    return W.Workload("mixed", buf, offs, lens, K, "")
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("default", {}),
+    ("all exact", {"l_samp_min": 1 << 30}),
+    ("small cap", {"cap": 3000}),
+    ("tiny cap", {"cap": 600}),
+    ("underfill", {"rho_num": 1, "rho_den": 2, "rho1_num": 3, "rho1_den": 4}),
+    ("no band margin", {"rho_num": 1, "rho_den": 1, "rho1_num": 1, "rho1_den": 1}),
+    ("stride 64", {"s_log2": 6, "l_samp_min": 4096}),
+    ("stride 1", {"s_log2": 0, "l_samp_min": 4096}),
+    ("stride 4096", {"s_log2": 12, "l_samp_min": 0}),
+])
+def test_forced_routes(topk, name, kw):
+    pol = topk.default_policy()
+    for k, v in kw.items():
+        setattr(pol, k, v)
+    for wl in (_mixed(), W.adversarial(n_rows=96)):
+        parity(topk, wl, policy=pol, where=f"{wl.name} / {name}")
+
+
+# ----------------------------------------------------------- edge cases --
+
+def _edge_workload():
+    rng = np.random.default_rng(13)
+    sub1 = np.array([1], np.uint32).view(np.float32)[0]
+    specials = np.array([0.0, -0.0, np.inf, -np.inf, sub1, -sub1, 1.0, -1.0], np.float32)
+    rows = [np.zeros(0, np.float32), rng.standard_normal(1).astype(np.float32),
+            rng.standard_normal(255).astype(np.float32), rng.standard_normal(256).astype(np.float32),
+            rng.standard_normal(257).astype(np.float32),
+            specials[rng.integers(0, 8, 5000)],
+            specials[rng.integers(0, 8, 40000)],
+            np.full(9000, -np.inf, np.float32),
+            np.full(9000, -0.0, np.float32),
+            np.concatenate([np.full(4000, 0.0, np.float32), np.full(6000, -0.0, np.float32)]),
+            (rng.standard_normal(33333) * 1e-40).astype(np.float32)]  # subnormals
+    lens = [r.size for r in rows] + [-5]
+    rows.append(np.zeros(0, np.float32))
+    # unaligned packing: odd gaps between rows
+    parts, offs, pos = [], [], 0
+    for r in rows:
+        gap = int(rng.integers(0, 4))
+        parts.append(rng.standard_normal(gap).astype(np.float32))
+        pos += gap
+        offs.append(pos)
+        parts.append(r)
+        pos += r.size
+    buf = np.concatenate(parts)
+    return W.Workload("edges", buf, np.array(offs, np.int64), np.array(lens, np.int32), 256, "")
+
+
+def test_edge_rows(topk):
+    wl = _edge_workload()
+    parity(topk, wl)
+    import torch
+
+    s, o, l = device_arrays(wl)
+    gi, gv, _, _ = run_hip(s, o, l, wl.K, topk.default_policy(), False)
+    for r in range(wl.n_rows):
+        check_row(wl.row(r), wl.K, gi[r], gv[r], f"edge row {r}")
+
+
+def test_padded_pitch_rows(topk):
+    rng = np.random.default_rng(17)
+    n, pitch = 48, 70001
+    buf = rng.standard_normal(n * pitch).astype(np.float32)
+    lens = rng.integers(0, pitch + 1, n).astype(np.int32)
+    wl = W.Workload("pitch", buf, (np.arange(n) * pitch).astype(np.int64), lens, 2048, "")
+    parity(topk, wl)
+
+
+def test_long_tie_row_uses_index_digits(topk):
+    """2.5M equal values: the boundary bin exceeds the frontier (re-read path)
+    and the tie is broken on all three index digits."""
+    rng = np.random.default_rng(19)
+    a = np.full(2_500_000, 0.75, np.float32)
+    b = rng.standard_normal(3_000_000).astype(np.float32)
+    b[rng.choice(b.size, 3000, replace=False)] = 9.0                    # 3000 ties at the top
+    buf = np.concatenate([a, b])
+    wl = W.Workload("long ties", buf, np.array([0, a.size], np.int64),
+                    np.array([a.size, b.size], np.int32), 2048, "")
+    gt, st = parity(topk, wl)
+    assert st["reread"] >= 1
+
+
+def test_zero_rows_noop(topk):
+    import torch
+
+    say("zero rows")
+    ws = topk.alloc_workspace(4, 16)
+    e = torch.empty(0, device="cuda")
+    topk.topk_ragged(e, torch.empty(0, dtype=torch.int64, device="cuda"),
+                     torch.empty(0, dtype=torch.int32, device="cuda"), 0, 16,
+                     torch.empty(0, dtype=torch.int32, device="cuda"), e, ws)
+    torch.cuda.synchronize()
+
+
+def test_workspace_too_small_is_flagged(topk):
+    import torch
+
+    wl = W.decode(n_rows=8)
+    say("workspace for 4 rows, call with 8")
+    s, o, l = device_arrays(wl)
+    ws = topk.alloc_workspace(4, wl.K)
+    gi, gv, _, st = run_hip(s, o, l, wl.K, None, False, ws=ws)
+    assert st["errors"] == 1
+    assert np.all(gi == -1) and np.all(np.isneginf(gv))
+
+
+def test_repeated_calls_are_stable(topk):
+    """Split rows reuse per-row state: 30 calls on one workspace must agree."""
+    import torch
+
+    wl = W.decode()
+    say("decode x30")
+    s, o, l = device_arrays(wl)
+    ws = topk.alloc_workspace(wl.n_rows, wl.K)
+    oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, wl.K)
+    for it in range(30):
+        gi, gv, _, st = run_hip(s, o, l, wl.K, None, False, ws=ws)
+        assert_same_selection(gi, gv, oi, ov, where=f"decode call {it}")
+
+
+def test_graph_capture_and_replay(topk):
+    """Three calls (two workloads) captured in one HIP graph, replayed with host
+    work and synchronisation between replays; every replay must match the
+    eager results."""
+    import torch
+
+    wa, wb = W.decode(), W.adversarial(n_rows=128)
+    say("graph replay")
+    sa, oa, la = device_arrays(wa)
+    sb, ob, lb = device_arrays(wb)
+    K = 2048
+    wsa = topk.alloc_workspace(wa.n_rows, K)
+    wsb = topk.alloc_workspace(wb.n_rows, K)
+    outs = [(torch.empty((wa.n_rows, K), dtype=torch.int32, device="cuda"),
+             torch.empty((wa.n_rows, K), dtype=torch.float32, device="cuda")),
+            (torch.empty((wb.n_rows, K), dtype=torch.int32, device="cuda"),
+             torch.empty((wb.n_rows, K), dtype=torch.float32, device="cuda")),
+            (torch.empty((wa.n_rows, K), dtype=torch.int32, device="cuda"),
+             torch.empty((wa.n_rows, K), dtype=torch.float32, device="cuda"))]
+    calls = [(sa, oa, la, wa.n_rows, wsa), (sb, ob, lb, wb.n_rows, wsb), (sa, oa, la, wa.n_rows, wsa)]
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for (s, o, l, n, ws), (oi, ov) in zip(calls, outs):       # warm-up, eager
+            topk.topk_ragged(s, o, l, n, K, oi, ov, ws, stream)
+    stream.synchronize()
+    eager = [(oi.cpu().numpy(), ov.cpu().numpy()) for oi, ov in outs]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for (s, o, l, n, ws), (oi, ov) in zip(calls, outs):
+            topk.topk_ragged(s, o, l, n, K, oi, ov, ws, torch.cuda.current_stream())
+    for rep in range(10):
+        for oi, ov in outs:
+            oi.fill_(-9)
+            ov.fill_(0.5)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for j, (oi, ov) in enumerate(outs):
+            assert_same_selection(oi.cpu().numpy(), ov.cpu().numpy(), *eager[j],
+                                  where=f"replay {rep} call {j}")
+    ri, rv = oracle.topk_ragged(wa.scores, wa.row_offsets, wa.row_lengths, K)
+    assert_same_selection(*eager[0], ri, rv, where="eager vs oracle")
