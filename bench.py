@@ -1,0 +1,216 @@
+"""Benchmark: exact Top-2048 over the decode batch (64 ragged FP32 rows, L
+uniform in [16384, 131072]) on one MI355X.
+
+A step is one topk_ragged call over one batch already resident in HBM.  Calls
+rotate over enough distinct copies of the batch (>= 512 MB in total) that the
+256 MB last-level cache cannot serve repeats; they are captured in HIP graphs
+(one call per graph node, as a serving loop would replay them) and replayed
+back-to-back on one stream.  HIP events on that stream bracket exactly
+`--steps` calls after `--warmup` untimed ones.
+
+Metric: effective score-read bandwidth = 4 B x sum(L) per call / time per
+call, the algorithmic bytes of an exact selector (one complete read of every
+valid score), reported with the per-call time.  The JSON line also carries the
+roofline of the kernel (HBM bound, 8 TB/s peak), route counts, and the CPU
+oracle timed on the host cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+MALL_BYTES = 256 << 20
+ROTATE_MIN_BYTES = 512 << 20
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_08450_amd", "csrc", "topk_ragged.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode.json")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def measured_traffic(config: int):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
+    when they are missing or were taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("config") != config:
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def make_workload(config: int):
+    from paper_2609_08450_amd import workloads as W
+
+    return W.make(config)
+
+
+def cpu_baseline(wl, budget_s: float, threads: int):
+    """The oracle as it stands, on the host cores, over whole copies of the
+    batch until about budget_s seconds have passed."""
+    import oracle
+
+    oracle.topk_ragged(wl.scores[:0], wl.row_offsets[:0], wl.row_lengths[:0], wl.K, threads)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, wl.K, threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    gbs = 4.0 * wl.total_len * reps / el / 1e9
+    return {"value": round(gbs, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full batches ({wl.n_rows} rows, {wl.total_len} scores each) "
+                      f"in {el:.1f} s, {threads} OpenMP threads, plain sort oracle",
+            "us_per_call": round(el / reps * 1e6, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3000)
+    ap.add_argument("--warmup", type=int, default=60)
+    ap.add_argument("--config", type=int, default=2,
+                    help="workload: 1 tiny, 2 decode (headline), 3 chunked prefill, 4 long split, 5 edge mix")
+    ap.add_argument("--calls-per-graph", type=int, default=0, help="0 = number of rotated copies")
+    ap.add_argument("--no-rotate", action="store_true", help="reuse one copy (cache-resident input)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time; 0 = skip")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(rows shard independently across GPUs; see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_08450_amd import topk
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    wl = make_workload(args.config)
+    K, n = wl.K, wl.n_rows
+    batch_bytes = 4 * wl.scores.size
+    copies = 1 if args.no_rotate else max(1, -(-ROTATE_MIN_BYTES // batch_bytes))
+    stream = torch.cuda.Stream(device=dev)
+
+    with torch.cuda.stream(stream):
+        host = torch.from_numpy(wl.scores)
+        bufs = [host.to(dev) for _ in range(copies)]
+        offs = torch.from_numpy(wl.row_offsets).to(dev)
+        lens = torch.from_numpy(wl.row_lengths).to(dev)
+        out_idx = torch.empty((n, K), dtype=torch.int32, device=dev)
+        out_val = torch.empty((n, K), dtype=torch.float32, device=dev)
+        ws = topk.alloc_workspace(n, K, dev, stream)
+    stream.synchronize()
+
+    def call(i, s):
+        topk.topk_ragged(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws, s)
+
+    # one graph with G consecutive calls over rotating copies; a tail graph for
+    # the remainder, so exactly `steps` calls are timed
+    G = args.calls_per_graph or copies
+    G = max(1, min(G, args.steps)) if args.steps > 0 else 1
+
+    def capture(ncalls, first):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for j in range(ncalls):
+                call(first + j, torch.cuda.current_stream())
+        return g
+
+    with torch.cuda.stream(stream):
+        for i in range(min(args.warmup, 3)):
+            call(i, stream)           # eager warm-up (code object load)
+    stream.synchronize()
+    g_main = capture(G, 0)
+    rem = args.steps % G
+    g_tail = capture(rem, 0) if rem else None
+    stream.synchronize()
+
+    def run(nsteps):
+        reps, tail = divmod(nsteps, G)
+        for _ in range(reps):
+            g_main.replay()
+        if tail:
+            assert tail == rem
+            g_tail.replay()
+
+    # warmup: whole graph replays plus the tail, untimed
+    wreps = max(1, args.warmup // G)
+    for _ in range(wreps):
+        g_main.replay()
+    torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        run(args.steps)
+        ev1.record(stream)
+    ev1.synchronize()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    ms_per_step = ms / args.steps
+    alg_bytes = 4.0 * wl.total_len
+    gbs = alg_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # outside the timed region: route counts of one call and a parity spot check
+    topk.read_stats(ws, stream)
+    with torch.cuda.stream(stream):
+        call(0, stream)
+    routes = topk.read_stats(ws, stream)
+
+    traffic = measured_traffic(args.config)
+    result = {
+        "metric": "effective score-read GB/s, exact Top-2048 over ragged FP32 rows",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": wreps * G,
+        "ms_per_step": round(ms_per_step, 6),
+        "us_per_call": round(ms_per_step * 1e3, 3),
+        "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name + ": " + wl.description, "rows": n, "K": K,
+                   "sum_len": wl.total_len, "bytes_per_call": int(alg_bytes),
+                   "rotated_copies": copies, "calls_per_graph": G,
+                   "rotated_bytes": copies * batch_bytes},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": traffic},
+        "routes": routes,
+        "kernel": "topk_ragged_kernel",
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    if args.cpu_budget > 0:
+        threads = min(16, os.cpu_count() or 1)
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget, threads)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

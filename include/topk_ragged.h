@@ -55,7 +55,7 @@ extern "C" {
  * the on-chip frontier of TOPK_FRONTIER_CAP entries). */
 #define TOPK_K_MAX 16384
 /* Frontier capacity of one workgroup, in (index, key) pairs. */
-#define TOPK_FRONTIER_CAP 8192
+#define TOPK_FRONTIER_CAP 6144
 /* Words per row written by topk_ragged_ex when row_trace is not NULL. */
 #define TOPK_TRACE_WORDS 8
 

@@ -116,7 +116,7 @@ def default_policy(**kw) -> Policy:
     """The pipeline constants of the evaluated configuration: s = 128,
     K~ = 1.5 K, K~1 = 1.75 K (Sections 4.2 and 6.4), plus the sampling floor
     and frontier capacity of this implementation."""
-    p = dict(s=128, rho_num=3, rho_den=2, rho1_num=7, rho1_den=4, l_samp_min=8192, cap=8192)
+    p = dict(s=128, rho_num=3, rho_den=2, rho1_num=7, rho1_den=4, l_samp_min=8192, cap=6144)
     p.update(kw)
     return Policy(**p)
 

@@ -26,6 +26,8 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <climits>
+#include <type_traits>
 
 #include "../../include/topk_ragged.h"
 
@@ -33,8 +35,15 @@ namespace {
 
 constexpr int kBlock = 512;                 // threads per workgroup (8 waves)
 constexpr int kBins = 2048;                 // 11-bit digits and coarse bins
-constexpr int kCap = TOPK_FRONTIER_CAP;     // LDS frontier capacity (pairs)
-constexpr int kVec = 4;                     // 16-byte loads per thread per chunk
+constexpr int kWaves = kBlock / 64;
+constexpr int kCap = TOPK_FRONTIER_CAP;     // largest policy frontier (pairs)
+constexpr int kFront = 7168;                // LDS frontier storage (pairs)
+constexpr int kWaveCap = kFront / kWaves - 1; // Phase 2 storage per wave (+1 spill slot)
+constexpr int kWaveStride = kFront / kWaves;
+static_assert(kCap <= kFront, "policy capacity must fit the storage");
+constexpr int kVec = 8;                     // 16-byte loads per thread per chunk
+static_assert(kVec * 4 <= 64, "per-thread element masks are 64-bit");
+static_assert(kFront % kBlock == 0 && kFront % kWaves == 0, "frontier layout");
 constexpr int kChunkVecs = kBlock * kVec;   // 16-byte vectors per chunk
 constexpr int kMaxSplit = 64;               // most segments per row
 constexpr int kSegMin = 8192;               // shortest segment, elements
@@ -42,21 +51,24 @@ constexpr uint32_t kMagic = 0x544F504Bu;    // workspace header tag
 constexpr int kSpinLimit = 1 << 15;         // polls before recomputing the view
 constexpr size_t kHeaderBytes = 1024;
 constexpr size_t kRowStateBytes = 256;
-constexpr size_t kRowBlockBytes = kRowStateBytes + 2 * kCap * sizeof(uint32_t);
+constexpr size_t kRowBlockBytes = kRowStateBytes + 2 * kFront * sizeof(uint32_t);
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-// Per-row state of a split row (32 bytes).  Row r of a split call owns the
-// workspace block at kHeaderBytes + r * kRowBlockBytes: this state, padded to
-// 256 bytes, then kCap candidate indices and kCap candidate keys.
+// Per-row state of a split row.  Row r of a split call owns the workspace
+// block at kHeaderBytes + r * kRowBlockBytes: this state, padded to 256
+// bytes, then kFront candidate indices and kFront candidate FP32 bit patterns
+// (the segments' A(tau1) entries, concatenated).
 struct RowState {
-    uint32_t flag;   // 1 once cut0/cut1/taus are published by segment 0
-    uint32_t cut0;   // ascending-key endpoint of tau0
-    uint32_t cut1;   // ascending-key endpoint of tau1
-    uint32_t taus;   // tau0 | tau1 << 16
-    uint32_t arrive; // segments done with Phase 2
-    uint32_t count;  // admitted candidates of the row (exact total)
-    uint32_t pad[2];
+    uint32_t flag;       // 1 once cut0/cut1/taus are published by segment 0
+    uint32_t cut0;       // ascending-key endpoint of tau0
+    uint32_t cut1;       // ascending-key endpoint of tau1
+    uint32_t taus;       // tau0 | tau1 << 16
+    uint32_t arrive;     // segments done with Phase 2
+    uint32_t count1;     // C(tau1) of the row (exact)
+    uint32_t count0;     // C(tau0) of the row (exact)
+    uint32_t stored;     // entries reserved in the candidate buffer
+    uint32_t incomplete; // a segment could not keep all of its A(tau1)
 };
 
 // Workspace header (first kHeaderBytes of the workspace).
@@ -87,7 +99,29 @@ struct KArgs {
     int32_t q0, q1;
     int32_t l_samp_min;
     int32_t cap;
+#ifdef TOPK_PHASE_TIMERS
+    uint64_t *timers; // 8 words per workgroup, see PHASE_MARK
+#endif
 };
+
+// Optional phase timers (built only with -DTOPK_PHASE_TIMERS): thread 0 of
+// each workgroup stamps the constant-rate clock at fixed points of the row
+// pipeline: 0 start, 1 endpoints known, 2 Phase 2 done, 3 arrived, 4 finisher
+// has the merged frontier, 5 row done; word 6 = hardware id, 7 = role.
+#ifdef TOPK_PHASE_TIMERS
+#define PHASE_MARK(a, k)                                                                 \
+    do {                                                                                 \
+        if ((a).timers && threadIdx.x == 0)                                              \
+            (a).timers[(size_t)blockIdx.x * 8 + (k)] = wall_clock64();                   \
+    } while (0)
+#define PHASE_WORD(a, k, v)                                                              \
+    do {                                                                                 \
+        if ((a).timers && threadIdx.x == 0) (a).timers[(size_t)blockIdx.x * 8 + (k)] = (v); \
+    } while (0)
+#else
+#define PHASE_MARK(a, k) do {} while (0)
+#define PHASE_WORD(a, k, v) do {} while (0)
+#endif
 
 // ------------------------------------------------------------- keys ----
 
@@ -174,6 +208,16 @@ __device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t *ctr) {
     return base + pre;
 }
 
+// Wave-aggregated append for a ballot mask already computed by the caller:
+// one LDS atomic per wave.  Every lane of the wave must call it.
+__device__ __forceinline__ uint32_t wave_append_bits(uint64_t m, uint32_t *ctr) {
+    const uint32_t pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    uint32_t base = 0;
+    if (lane_id() == 0) base = atomicAdd(ctr, (uint32_t)__popcll(m));
+    return __builtin_amdgcn_readfirstlane(base) + pre;
+}
+
 struct Find {
     uint32_t bin;   // first bin whose inclusive prefix reaches the target
     uint32_t below; // prefix before that bin
@@ -221,10 +265,13 @@ __device__ __forceinline__ void wave_find(const uint32_t *hist, uint32_t k0, uin
 
 struct alignas(16) Smem {
     uint32_t hist[kBins];
-    uint32_t ci[kCap];  // frontier indices (row-relative)
-    uint32_t ck[kCap];  // frontier kappa32 keys
+    uint32_t ci[kFront]; // frontier indices (row-relative)
+    uint32_t ck[kFront]; // frontier keys: FP32 bits after Phase 2, kappa32 after compaction
+    uint32_t wcnt[kWaves]; // Phase 2 hits per wave (exact, may exceed kWaveCap)
     Find find[2];
-    uint32_t cnt;       // candidates appended to ci/ck (exact, may exceed cap)
+    uint32_t cnt;       // C(tau1), or the append counter of the current pass
+    uint32_t cnt0;      // C(tau0)
+    uint32_t incomplete;
     uint32_t opos;      // outputs written for the current row
     uint32_t next;      // compaction counter in refinement
     uint32_t cut0, cut1, tau0, tau1;
@@ -248,50 +295,71 @@ __device__ __forceinline__ void clear_hist(Smem &sm) {
 // 16 values, the row index of each vector's first element, and the valid
 // row-index window [lo, hi).  Two chunks are in flight (ping-pong registers).
 
+typedef __attribute__((address_space(1))) const f4 gf4; // global, not flat
+
 template <bool kNonTemporal>
 __device__ __forceinline__ f4 load4(const f4 *p) {
-    if constexpr (kNonTemporal) return __builtin_nontemporal_load(p);
-    else return *p;
+    const gf4 *g = (const gf4 *)p;
+    if constexpr (kNonTemporal) return __builtin_nontemporal_load(g);
+    else return *g;
 }
 
-template <bool kNT, class F>
+struct NoPrologue {
+    __device__ void operator()() const {}
+};
+
+// Double-buffered chunks: while one chunk (kVec 16-byte loads per thread) is
+// consumed, the next one is in flight.  Loads are unconditional -- lanes and
+// chunks past the end re-read the last vector of the range (one cache line per
+// wave), masked by the window test -- so the in-order load counter lets each
+// consume wait for its own chunk only.  prologue() runs once, by every thread:
+// before the first issue when it loads from memory itself (its loads would
+// otherwise queue behind the chunk), else with the first chunk in flight.
+template <bool kNT, class F, class Pro = NoPrologue>
 __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int32_t beg,
-                                           int32_t end, F &&fn) {
-    if (beg >= end) return;
+                                           int32_t end, F &&fn, Pro &&prologue = Pro(),
+                                           bool prologue_first = false) {
+    if (beg >= end) {
+        prologue();
+        return;
+    }
     const uintptr_t sp = reinterpret_cast<uintptr_t>(scores);
     const int64_t sh = (int64_t)((sp & 15) >> 2);
     const int64_t v0 = (off + beg + sh) >> 2;
     const int32_t nvec = (int32_t)(((off + end + sh + 3) >> 2) - v0);
-    const f4 *vbase = reinterpret_cast<const f4 *>(sp & ~(uintptr_t)15) + v0;
-    const int32_t ibase = (int32_t)(v0 * 4 - sh - off); // row index of vbase[0].x
+    const char *vbase = reinterpret_cast<const char *>(sp & ~(uintptr_t)15) + v0 * 16;
+    const int32_t ibase = (int32_t)(v0 * 4 - sh - off); // row index of vbase's first element
+    const int32_t nch = (nvec + kChunkVecs - 1) / kChunkVecs;
     const int tid = threadIdx.x;
-    f4 a[kVec], b[kVec];
-    auto issue = [&](f4 *dst, int32_t cb) {
+    f4 xa[kVec], xb[kVec];
+    auto issue = [&](f4 *dst, int32_t c) {
+        const int32_t cb = c * kChunkVecs;
 #pragma unroll
         for (int m = 0; m < kVec; m++) {
-            const int32_t vi = cb + m * kBlock + tid;
-            dst[m] = (vi < nvec) ? load4<kNT>(vbase + vi) : f4{0.f, 0.f, 0.f, 0.f};
+            const int32_t vi = min(cb + m * kBlock + tid, nvec - 1);
+            dst[m] = load4<kNT>(reinterpret_cast<const f4 *>(vbase + (uint32_t)vi * 16u));
         }
     };
-    auto consume = [&](const f4 *src, int32_t cb) {
+    auto consume = [&](const f4 *src, int32_t c) {
+        if (c >= nch) return;
+        const int32_t cb = c * kChunkVecs;
+        // vectors of this chunk per thread (block-uniform)
+        const int32_t mv = min(kVec, (nvec - cb + kBlock - 1) / kBlock);
         int32_t i0[kVec];
 #pragma unroll
         for (int m = 0; m < kVec; m++) i0[m] = ibase + (cb + m * kBlock + tid) * 4;
-        fn(src, i0, beg, end);
+        // interior chunks need no per-element window test
+        const bool edge = ibase + cb * 4 < beg || ibase + (cb + mv * kBlock) * 4 > end;
+        fn(src, i0, beg, end, edge, mv);
     };
-    int32_t cb = 0;
-    issue(a, cb);
-    for (;;) {
-        const int32_t nb = cb + kChunkVecs;
-        if (nb < nvec) issue(b, nb);
-        consume(a, cb);
-        if (nb >= nvec) break;
-        cb = nb;
-        const int32_t na = cb + kChunkVecs;
-        if (na < nvec) issue(a, na);
-        consume(b, cb);
-        if (na >= nvec) break;
-        cb = na;
+    if (prologue_first) prologue();
+    issue(xa, 0);
+    if (!prologue_first) prologue();
+    for (int32_t c = 0; c < nch; c += 2) {
+        issue(xb, c + 1);
+        consume(xa, c);
+        issue(xa, c + 2);
+        consume(xb, c + 1);
     }
 }
 
@@ -309,25 +377,25 @@ __device__ __forceinline__ void collect_range(Smem &sm, const float *scores, int
                               int32_t end, uint32_t lo_key, uint32_t hi_key, bool hi_inclusive,
                               uint32_t cap) {
     stream_row<kNT>(scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                               int32_t hi) {
-        uint32_t mask = 0;
+                                               int32_t hi, bool, int32_t mv) {
+        uint64_t mask = 0; // one bit per element of the chunk (kVec * 4 <= 64)
 #pragma unroll
-        for (int m = 0; m < kVec; m++) {
+        for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
                 const uint32_t u = asc_key(fbits(x[m][c]));
                 const bool ok = u >= lo_key && (hi_inclusive ? u <= hi_key : u < hi_key) &&
                                 in_window(i0[m] + c, lo, hi);
-                mask |= (ok ? 1u : 0u) << (m * 4 + c);
+                mask |= (ok ? 1ull : 0ull) << (m * 4 + c);
             }
         }
         if (mask) {
-            uint32_t pos = atomicAdd(&sm.cnt, (uint32_t)__popc(mask));
+            uint32_t pos = atomicAdd(&sm.cnt, (uint32_t)__popcll(mask));
 #pragma unroll
-            for (int m = 0; m < kVec; m++) {
+            for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
                 for (int c = 0; c < 4; c++) {
-                    if (mask & (1u << (m * 4 + c))) {
+                    if (mask & (1ull << (m * 4 + c))) {
                         if (pos < cap) {
                             sm.ci[pos] = (uint32_t)(i0[m] + c);
                             sm.ck[pos] = ~asc_key(fbits(x[m][c]));
@@ -338,6 +406,153 @@ __device__ __forceinline__ void collect_range(Smem &sm, const float *scores, int
             }
         }
     });
+}
+
+// Phase 2 over [beg, end) (Section 4.3): certify against cut0 and keep the
+// admitted tail.  Every value with ascending key u >= cut1 (the nested
+// boundary, so a C(tau0) < K proposal can take the band of
+// eq:method:rescue-band without a second traversal) is stored as (index, FP32
+// bits) in the private region of its wave: sm.ci/ck[w * kWaveCap ..), in
+// element order within the wave.  Each element costs one compare; a
+// wave-wide ballot places the hits with no atomics.  C(tau1) and C(tau0) are
+// counted exactly even where a wave region overflows (sm.incomplete is then
+// set).  The endpoints are read from sm after prologue() has run.
+template <class Pro>
+__device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, int64_t off,
+                                               int32_t beg, int32_t end, bool prologue_first,
+                                               Pro &&prologue) {
+    const int w = threadIdx.x >> 6;
+    uint32_t cur = 0; // wave-uniform: hits so far
+    stream_row<true>(
+        scores, off, beg, end,
+        [&](const f4 *x, const int32_t *i0, int32_t lo, int32_t hi, bool edge, int32_t mv) {
+            const uint32_t cut1 = sm.cut1;
+            uint32_t *wi = sm.ci + w * kWaveStride;
+            uint32_t *wk = sm.ck + w * kWaveStride;
+            auto run = [&](auto positive, auto edge_chunk) {
+                constexpr bool kPos = decltype(positive)::value;
+                constexpr bool kEdge = decltype(edge_chunk)::value;
+                // A positive endpoint v: x >= v iff the raw FP32 bits, read as
+                // signed integers, compare >= (one integer compare).
+                const int32_t t1 = (int32_t)bits_from_asc(cut1);
+#pragma unroll
+                for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+                    for (int c = 0; c < 4; c++) {
+                        const uint32_t b = fbits(x[m][c]);
+                        const bool h1 = kPos ? (int32_t)b >= t1 : asc_key(b) >= cut1;
+                        bool hit = h1;
+                        if constexpr (kEdge) hit = h1 && in_window(i0[m] + c, lo, hi);
+                        const uint64_t m1 = __ballot(hit);
+                        if (m1) {
+                            // slot kWaveCap of the region absorbs hits past its
+                            // capacity (the count stays exact)
+                            const uint32_t q = min(cur + __builtin_amdgcn_mbcnt_hi(
+                                                             (uint32_t)(m1 >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m1, 0u)),
+                                                   (uint32_t)kWaveCap);
+                            if (hit) { wi[q] = (uint32_t)(i0[m] + c); wk[q] = b; }
+                            cur += (uint32_t)__popcll(m1);
+                        }
+                    }
+                }
+            };
+            // four specialisations, chosen once per chunk
+            if (cut1 > 0x80000000u) {
+                if (edge) run(std::true_type{}, std::true_type{});
+                else run(std::true_type{}, std::false_type{});
+            } else {
+                if (edge) run(std::false_type{}, std::true_type{});
+                else run(std::false_type{}, std::false_type{});
+            }
+        },
+        prologue, prologue_first);
+    if ((threadIdx.x & 63) == 0) {
+        sm.wcnt[w] = cur;
+        atomicAdd(&sm.cnt, cur);
+        if (cur > (uint32_t)kWaveCap) sm.incomplete = 1u;
+    }
+}
+
+// C(tau0) from the stored entries of Phase 2 (all of A(tau1) when complete).
+// Ends with a barrier.
+__device__ __forceinline__ uint32_t count_tail(Smem &sm, bool segmented, uint32_t n,
+                                               uint32_t kmin) {
+    uint32_t c = 0;
+    for (uint32_t t = threadIdx.x; t < (uint32_t)kFront; t += kBlock) {
+        bool v;
+        if (segmented) {
+            const uint32_t w = t / kWaveStride;
+            v = (t - w * kWaveStride) < min(sm.wcnt[w], (uint32_t)kWaveCap);
+        } else {
+            v = t < n;
+        }
+        c += (v && asc_key(sm.ck[t]) >= kmin) ? 1u : 0u;
+    }
+    c = wave_incl_scan(c);
+    if ((threadIdx.x & 63) == 63 && c) atomicAdd(&sm.cnt0, c);
+    __syncthreads();
+    return sm.cnt0;
+}
+
+// C(tau0) of row elements [beg, end) by re-reading them (overflow fallback).
+// sm.cnt0 must be zero on entry.  Ends with a barrier.
+__device__ __forceinline__ uint32_t count_range(Smem &sm, const float *scores, int64_t off,
+                                                int32_t beg, int32_t end, uint32_t kmin) {
+    uint32_t c = 0;
+    stream_row<false>(scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                                 int32_t hi, bool, int32_t mv) {
+#pragma unroll
+        for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+            for (int cc = 0; cc < 4; cc++)
+                c += (in_window(i0[m] + cc, lo, hi) && asc_key(fbits(x[m][cc])) >= kmin) ? 1u : 0u;
+        }
+    });
+    c = wave_incl_scan(c);
+    if ((threadIdx.x & 63) == 63 && c) atomicAdd(&sm.cnt0, c);
+    __syncthreads();
+    return sm.cnt0;
+}
+
+// Rewrites the stored entries as a contiguous frontier of (index, kappa32)
+// holding only the values with ascending key >= kmin: A(tau0) for a certified
+// proposal (kmin = cut0), A(tau1) for the band (kmin = cut1).  The source is
+// either the per-wave regions of Phase 2 (segmented) or [0, n) (contiguous),
+// both holding FP32 bits.  Entries are staged in registers, so the rewrite
+// is in place.  Returns the new count; ends with a barrier.
+__device__ __forceinline__ uint32_t compact_frontier(Smem &sm, bool segmented, uint32_t n,
+                                                     uint32_t kmin) {
+    constexpr int kPer = kFront / kBlock;
+    const int tid = threadIdx.x;
+    uint32_t ri[kPer], rb[kPer];
+    bool rv[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const uint32_t t = (uint32_t)(j * kBlock + tid);
+        bool v;
+        if (segmented) {
+            const uint32_t w = t / kWaveStride;
+            v = (t - w * kWaveStride) < min(sm.wcnt[w], (uint32_t)kWaveCap);
+        } else {
+            v = t < n;
+        }
+        ri[j] = v ? sm.ci[t] : 0u;
+        rb[j] = v ? sm.ck[t] : 0u;
+        rv[j] = v && asc_key(rb[j]) >= kmin;
+    }
+    if (tid == 0) sm.next = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const uint32_t q = wave_append(rv[j], &sm.next);
+        if (rv[j]) {
+            sm.ci[q] = ri[j];
+            sm.ck[q] = ~asc_key(rb[j]);
+        }
+    }
+    __syncthreads();
+    return sm.next;
 }
 
 // ----------------------------------------------------------- outputs ----
@@ -460,9 +675,9 @@ __device__ __forceinline__ void reread_select(const KArgs a, Smem &sm, int r, in
         __syncthreads();
         const uint64_t hi_mask = (shift_done >= 64) ? 0ull : (~0ull << shift_done);
         stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                 int32_t hi) {
+                                                 int32_t hi, bool, int32_t mv) {
 #pragma unroll
-            for (int m = 0; m < kVec; m++) {
+            for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
                 for (int c = 0; c < 4; c++) {
                     const int32_t i = i0[m] + c;
@@ -491,9 +706,9 @@ __device__ __forceinline__ void reread_select(const KArgs a, Smem &sm, int r, in
     }
     // Output pass: every boundary-bin element with composite key <= T.
     stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                             int32_t hi) {
+                                             int32_t hi, bool, int32_t mv) {
 #pragma unroll
-        for (int m = 0; m < kVec; m++) {
+        for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
                 const int32_t i = i0[m] + c;
@@ -518,9 +733,9 @@ __device__ __forceinline__ void exact_classify(const KArgs a, Smem &sm, int r, i
     const int tid = threadIdx.x;
     const float *scores = a.scores;
     stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                      int32_t hi) {
+                                                      int32_t hi, bool, int32_t mv) {
 #pragma unroll
-        for (int m = 0; m < kVec; m++) {
+        for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++)
                 if (in_window(i0[m] + c, lo, hi)) atomicAdd(&sm.hist[coarse_bin(x[m][c])], 1u);
@@ -533,9 +748,9 @@ __device__ __forceinline__ void exact_classify(const KArgs a, Smem &sm, int r, i
     const uint32_t tstar = sm.find[0].bin;
     const bool fits = sm.find[0].eq <= (uint32_t)a.cap;
     stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                      int32_t hi) {
+                                                      int32_t hi, bool, int32_t mv) {
 #pragma unroll
-        for (int m = 0; m < kVec; m++) {
+        for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
                 const int32_t i = i0[m] + c;
@@ -611,19 +826,22 @@ __device__ __forceinline__ void phase1(const KArgs a, Smem &sm, int r, const flo
 // ---------------------------------------------------------- finish ----
 
 // Certification and the routes after Phase 2 (Section 4.3).  For a sampled
-// row sm.ci/ck hold the first min(C0, cap) entries of A(tau0) and C0 is the
-// exact admitted count: C0 >= K certifies the proposal (Lemma
-// lem:method:containment); C0 < K tries the band up to tau1
-// (eq:method:rescue-band); what is still underfilled, or does not fit the
-// frontier, runs exact coarse recovery (eq:method:exact-init).  Every route
-// then enters the same refinement with (E0 in the output, Q0 in LDS, k0).
-// Also counts the route and writes the trace.
-__device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64_t off, int64_t L, int64_t nv,
-                           bool sampled, uint32_t C0) {
+// row, C0 = C(tau0) and C1 = C(tau1) are exact and the stored entries hold
+// A(tau1) (per-wave regions if `segmented`, else [0, nstored)), complete
+// unless `incomplete`.  C0 >= K certifies the proposal (Lemma
+// lem:method:containment); C0 < K takes the band up to tau1
+// (eq:method:rescue-band) when that suffices; what is still underfilled, or
+// does not fit the frontier, runs exact coarse recovery (eq:method:exact-init).
+// Every route then enters the same refinement with (E0 in the output, Q0 in
+// LDS, k0).  An incomplete store is made up by re-reading the row for the
+// tail the route needs.  Also counts the route and writes the trace.
+__device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64_t off, int64_t L,
+                                           int64_t nv, bool sampled, uint32_t C0, uint32_t C1,
+                                           bool incomplete, bool segmented, uint32_t nstored) {
     const uint32_t K = (uint32_t)a.K;
     const uint32_t cap = (uint32_t)a.cap;
-    int32_t C1 = -1, tstar = -1, nq = -1;
-    uint32_t route, n_ref = 0, k_ref = K;
+    int32_t trC1 = -1, tstar = -1, nq = -1;
+    uint32_t route, n_ref = 0, k_ref = K, kmin = 0;
     clear_hist(sm);
     if (threadIdx.x == 0) sm.opos = 0;
     __syncthreads();
@@ -632,22 +850,30 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     } else if (C0 >= K && C0 <= cap) {
         route = TOPK_ROUTE_PRIMARY;
         n_ref = C0;
+        kmin = sm.cut0;
     } else if (C0 < K) {
-        // Band extension: append tau0 < c <= tau1, i.e. cut1 <= u < cut0.
-        if (threadIdx.x == 0) sm.cnt = C0;
-        __syncthreads();
-        collect_range<false>(sm, a.scores, off, 0, (int32_t)L, sm.cut1, sm.cut0, false, cap);
-        __syncthreads();
-        const uint32_t c1 = sm.cnt;
-        C1 = (int32_t)c1;
-        if (c1 >= K && c1 <= cap) {
+        trC1 = (int32_t)C1;
+        if (C1 >= K && C1 <= cap) {
             route = TOPK_ROUTE_BAND;
-            n_ref = c1;
+            n_ref = C1;
+            kmin = sm.cut1;
         } else {
-            route = (c1 < K) ? TOPK_ROUTE_EXACT_UNDERFILL : TOPK_ROUTE_EXACT_OVERFLOW;
+            route = (C1 < K) ? TOPK_ROUTE_EXACT_UNDERFILL : TOPK_ROUTE_EXACT_OVERFLOW;
         }
     } else {
         route = TOPK_ROUTE_EXACT_OVERFLOW;
+    }
+    if (n_ref) {
+        // Frontier of the certified tail: A(tau0), or A(tau1) for the band.
+        if (!incomplete) {
+            compact_frontier(sm, segmented, nstored, kmin);
+        } else {
+            if (threadIdx.x == 0) sm.cnt = 0;
+            __syncthreads();
+            collect_range<false>(sm, a.scores, off, 0, (int32_t)L, kmin, 0xFFFFFFFFu, true, cap);
+            __syncthreads();
+        }
+        nq = (int32_t)n_ref;
     }
     if (route >= TOPK_ROUTE_EXACT_UNSAMPLED) {
         exact_classify(a, sm, r, off, L);
@@ -661,8 +887,6 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
             route |= TOPK_ROUTE_REREAD_FLAG;
             reread_select(a, sm, r, off, L, f.bin, k_ref);
         }
-    } else {
-        nq = (int32_t)n_ref;
     }
     if (n_ref) refine(a, sm, r, n_ref, k_ref, L);
     if (threadIdx.x == 0) {
@@ -672,14 +896,15 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
             int32_t *t = a.trace + (int64_t)r * TOPK_TRACE_WORDS;
             t[0] = (int32_t)route; t[1] = (int32_t)nv;
             t[2] = sampled ? (int32_t)sm.tau0 : -1; t[3] = sampled ? (int32_t)sm.tau1 : -1;
-            t[4] = sampled ? (int32_t)C0 : -1; t[5] = C1; t[6] = tstar; t[7] = nq;
+            t[4] = sampled ? (int32_t)C0 : -1; t[5] = trC1; t[6] = tstar; t[7] = nq;
         }
     }
 }
 
 // ----------------------------------------------------------- kernel ----
 
-__global__ __launch_bounds__(kBlock) void topk_ragged_kernel(KArgs a) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void
+topk_ragged_kernel(KArgs a) {
     __shared__ Smem sm;
     const int tid = threadIdx.x;
     const int item = blockIdx.x;
@@ -689,6 +914,8 @@ __global__ __launch_bounds__(kBlock) void topk_ragged_kernel(KArgs a) {
     const int64_t L = (int64_t)max(a.lens[r], 0);
     const int64_t off = a.offs[r];
     const float *row = a.scores + off;
+    PHASE_MARK(a, 0);
+    PHASE_WORD(a, 6, (uint64_t)__smid());
 
     // Workspace check: a split plan needs per-row state for every row.
     const WsHeader *hdr = a.hdr;
@@ -734,86 +961,119 @@ __global__ __launch_bounds__(kBlock) void topk_ragged_kernel(KArgs a) {
     RowState *rs = reinterpret_cast<RowState *>(a.rows + (size_t)r * kRowBlockBytes);
     uint32_t *gi = reinterpret_cast<uint32_t *>(a.rows + (size_t)r * kRowBlockBytes +
                                                 kRowStateBytes);
-    uint32_t *gk = gi + kCap;
-    const uint32_t cap = (uint32_t)a.cap;
-    uint32_t C0 = 0;
+    uint32_t *gk = gi + kFront;
+    uint32_t C0 = 0, C1 = 0, nstored = 0;
+    bool incomplete = false, segmented = true;
 
     if (sampled) {
-        // Phase 1: segment 0 (or the only segment) builds the view; other
-        // segments wait for its published endpoints and rebuild the same view
+        // Phase 1 runs while the first chunk of this segment is loading:
+        // segment 0 (or the only segment) builds the view; other segments
+        // wait for its published endpoints and rebuild the same view
         // themselves if it does not arrive within the spin limit.
-        bool own_view = !split || p == 0;
-        if (!own_view) {
-            if (tid == 0) {
-                uint32_t f = 0;
-                for (int spin = 0; spin < kSpinLimit; spin++) {
-                    f = __hip_atomic_load(&rs->flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-                    if (f) break;
-                    __builtin_amdgcn_s_sleep(2);
-                }
-                sm.flag = f;
-                if (f) {
-                    sm.cut0 = __hip_atomic_load(&rs->cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    sm.cut1 = __hip_atomic_load(&rs->cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    const uint32_t taus =
-                        __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    sm.tau0 = taus & 0xFFFFu;
-                    sm.tau1 = taus >> 16;
-                } else {
-                    atomicAdd(&a.hdr->stats[kStatWaitFallback], 1u);
-                }
-            }
-            __syncthreads();
-            own_view = sm.flag == 0;
-        }
-        if (own_view) phase1(a, sm, r, row, L);
-        if (split && p == 0 && tid == 0) {
-            __hip_atomic_store(&rs->cut0, sm.cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&rs->cut1, sm.cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&rs->taus, sm.tau0 | (sm.tau1 << 16), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&rs->flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        }
-
-        // Phase 2 over this segment: certify against cut0 and compact A(tau0).
-        if (tid == 0) sm.cnt = 0;
-        __syncthreads();
+        if (tid == 0) { sm.cnt = 0; sm.cnt0 = 0; sm.incomplete = 0; }
         const int32_t beg = (int32_t)(p * seg);
         const int32_t end = (int32_t)min(L, p * seg + seg);
-        collect_range<true>(sm, a.scores, off, beg, end, sm.cut0, 0xFFFFFFFFu, true, cap);
+        auto endpoints = [&]() {
+            bool own_view = !split || p == 0;
+            if (!own_view) {
+                if (tid == 0) {
+                    // Relaxed polls (an acquire per poll would invalidate this
+                    // XCD's L2 every time); one acquire once the flag is set.
+                    uint32_t f = 0;
+                    for (int spin = 0; spin < kSpinLimit; spin++) {
+                        f = __hip_atomic_load(&rs->flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (f) break;
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+                    sm.flag = f;
+                    if (f) {
+                        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                        sm.cut0 = __hip_atomic_load(&rs->cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        sm.cut1 = __hip_atomic_load(&rs->cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        const uint32_t taus =
+                            __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        sm.tau0 = taus & 0xFFFFu;
+                        sm.tau1 = taus >> 16;
+                    } else {
+                        atomicAdd(&a.hdr->stats[kStatWaitFallback], 1u);
+                    }
+                }
+                __syncthreads();
+                own_view = sm.flag == 0;
+            }
+            if (own_view) phase1(a, sm, r, row, L);
+            if (split && p == 0 && tid == 0) {
+                __hip_atomic_store(&rs->cut0, sm.cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&rs->cut1, sm.cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&rs->taus, sm.tau0 | (sm.tau1 << 16), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&rs->flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            PHASE_MARK(a, 1);
+        };
+        // Phase 2 over this segment: certify against cut0 and keep A(tau1).
+        phase2_collect(sm, a.scores, off, beg, end, /*prologue_first=*/!split || p == 0,
+                       endpoints);
         __syncthreads();
-        C0 = sm.cnt;
+        C1 = sm.cnt;
+        incomplete = sm.incomplete != 0;
+        // C(tau0): from the stored A(tau1) entries, or by re-reading this
+        // segment when a wave region overflowed.
+        C0 = incomplete ? count_range(sm, a.scores, off, beg, end, sm.cut0)
+                        : count_tail(sm, true, 0, sm.cut0);
+        PHASE_MARK(a, 2);
+        PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)P << 16) | ((uint64_t)r << 32));
 
         if (split) {
-            // Publish this segment's candidates into the row's range
-            // (eq:method:split-local), then arrive; the last arrival merges
-            // (eq:method:split-reduce) and finishes the row.
+            // Publish this segment's entries and counts (eq:method:split-local),
+            // then arrive; the last arrival merges them (eq:method:split-reduce)
+            // and finishes the row.
+            uint32_t pre[kWaves + 1];
+            pre[0] = 0;
+#pragma unroll
+            for (int w = 0; w < kWaves; w++) pre[w + 1] = pre[w] + min(sm.wcnt[w], (uint32_t)kWaveCap);
             if (tid == 0) {
-                sm.base = C0 ? __hip_atomic_fetch_add(&rs->count, C0, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT)
-                             : 0u;
+                sm.base = pre[kWaves] ? __hip_atomic_fetch_add(&rs->stored, pre[kWaves],
+                                                               __ATOMIC_RELAXED,
+                                                               __HIP_MEMORY_SCOPE_AGENT)
+                                      : 0u;
+                if (C1) __hip_atomic_fetch_add(&rs->count1, C1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (C0) __hip_atomic_fetch_add(&rs->count0, C0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (incomplete)
+                    __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             __syncthreads();
             const uint32_t base = sm.base;
-            const uint32_t stored = min(C0, cap);
-            for (uint32_t t = tid; t < stored; t += kBlock) {
-                const uint32_t d = base + t;
-                if (d < cap) { gi[d] = sm.ci[t]; gk[d] = sm.ck[t]; }
+            for (uint32_t t = tid; t < (uint32_t)kFront; t += kBlock) {
+                const uint32_t w = t / kWaveStride, j = t - w * kWaveStride;
+                if (j < pre[w + 1] - pre[w]) {
+                    const uint32_t d = base + pre[w] + j;
+                    if (d < (uint32_t)kFront) { gi[d] = sm.ci[t]; gk[d] = sm.ck[t]; }
+                }
             }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            // Every wave waits for its own stores to reach L2; after the
+            // barrier one thread writes the L2 back for the other XCDs
+            // (agent-scope release) and arrives.
+            __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid == 0) {
-                const uint32_t old = __hip_atomic_fetch_add(&rs->arrive, 1u, __ATOMIC_ACQ_REL,
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                const uint32_t old = __hip_atomic_fetch_add(&rs->arrive, 1u, __ATOMIC_RELAXED,
                                                             __HIP_MEMORY_SCOPE_AGENT);
-                sm.flag = (old == (uint32_t)(P - 1)) ? 2u : 0u;
+                const bool last = old == (uint32_t)(P - 1);
+                if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                sm.flag = last ? 2u : 0u;
             }
             __syncthreads();
+            PHASE_MARK(a, 3);
             if (sm.flag != 2u) return;
 
             // Finisher.  Segment 0 published the endpoints before arriving.
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (tid == 0) {
-                sm.cnt = __hip_atomic_load(&rs->count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                sm.cnt = __hip_atomic_load(&rs->count1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                sm.cnt0 = __hip_atomic_load(&rs->count0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                sm.base = __hip_atomic_load(&rs->stored, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                sm.incomplete = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.cut0 = __hip_atomic_load(&rs->cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.cut1 = __hip_atomic_load(&rs->cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 const uint32_t taus =
@@ -822,21 +1082,30 @@ __global__ __launch_bounds__(kBlock) void topk_ragged_kernel(KArgs a) {
                 sm.tau1 = taus >> 16;
             }
             __syncthreads();
-            C0 = sm.cnt;
-            const uint32_t nload = min(C0, cap);
-            for (uint32_t t = tid; t < nload; t += kBlock) {
+            C1 = sm.cnt;
+            C0 = sm.cnt0;
+            const uint32_t stored = sm.base;
+            incomplete = sm.incomplete != 0 || stored > (uint32_t)kFront;
+            nstored = min(stored, (uint32_t)kFront);
+            segmented = false;
+            for (uint32_t t = tid; t < nstored; t += kBlock) {
                 sm.ci[t] = gi[t];
                 sm.ck[t] = gk[t];
             }
             __syncthreads();
+            PHASE_MARK(a, 4);
         }
     }
 
-    finish_row(a, sm, r, off, L, nv, sampled, C0);
+    finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored);
+    PHASE_MARK(a, 5);
 
     if (split && tid == 0) {
         // Leave the row state zeroed for the next call (graph replays).
-        __hip_atomic_store(&rs->count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rs->count1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rs->count0, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rs->stored, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&rs->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&rs->flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -966,6 +1235,16 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
 }
 
+#ifdef TOPK_PHASE_TIMERS
+static uint64_t *g_timers = nullptr;
+// Debug builds only: device buffer of 8 x (grid size) words for the next calls
+// (NULL disables).
+extern "C" int topk_ragged_debug_set_timers(uint64_t *buf) {
+    g_timers = buf;
+    return TOPK_OK;
+}
+#endif
+
 int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
                    int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                    const topk_ragged_policy *policy, int32_t *row_trace, void *stream) {
@@ -999,6 +1278,9 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     a.q1 = sample_rank(K, pol.rho1_num, pol.rho1_den, pol.s_log2);
     if (a.q1 < a.q0) a.q1 = a.q0;
     const int64_t floor_k = -(int64_t)pol.l_samp_min * K;
+#ifdef TOPK_PHASE_TIMERS
+    a.timers = g_timers;
+#endif
     a.l_samp_min = pol.l_samp_min >= 0 ? pol.l_samp_min
                                        : (int32_t)(floor_k < 0x7FFFFFFF ? floor_k : 0x7FFFFFFF);
     a.cap = pol.cap;

@@ -17,7 +17,7 @@ from .build import LIB_PATH
 
 TRACE_WORDS = 8
 K_MAX = 16384
-FRONTIER_CAP = 8192
+FRONTIER_CAP = 6144
 ROUTE_NAMES = ["direct", "primary", "band", "exact_unsampled", "exact_underfill", "exact_overflow"]
 
 

@@ -66,7 +66,7 @@ def test_policy_checks(lib):
 
     pol = topk.default_policy()
     P = ctypes.c_void_p(16)
-    for field, value in (("s_log2", 13), ("s_log2", -1), ("cap", 0), ("cap", 8193),
+    for field, value in (("s_log2", 13), ("s_log2", -1), ("cap", 0), ("cap", 6145),
                          ("rho_den", 0), ("rho1_num", 0)):
         p = topk.default_policy()
         setattr(p, field, value)
