@@ -100,23 +100,25 @@ struct KArgs {
     int32_t l_samp_min;
     int32_t cap;
 #ifdef TOPK_PHASE_TIMERS
-    uint64_t *timers; // 8 words per workgroup, see PHASE_MARK
+    uint64_t *timers; // 16 words per workgroup, see PHASE_MARK
 #endif
 };
 
 // Optional phase timers (built only with -DTOPK_PHASE_TIMERS): thread 0 of
 // each workgroup stamps the constant-rate clock at fixed points of the row
 // pipeline: 0 start, 1 endpoints known, 2 Phase 2 done, 3 arrived, 4 finisher
-// has the merged frontier, 5 row done; word 6 = hardware id, 7 = role.
+// has the merged frontier, 5 row done; word 6 = hardware id, 7 = role;
+// 8 finish entered, 9 frontier ready, 10..12 after refinement rounds 0..2,
+// 13 refinement done, 14 live entries entering refinement, 15 rounds run.
 #ifdef TOPK_PHASE_TIMERS
 #define PHASE_MARK(a, k)                                                                 \
     do {                                                                                 \
         if ((a).timers && threadIdx.x == 0)                                              \
-            (a).timers[(size_t)blockIdx.x * 8 + (k)] = wall_clock64();                   \
+            (a).timers[(size_t)blockIdx.x * 16 + (k)] = wall_clock64();                   \
     } while (0)
 #define PHASE_WORD(a, k, v)                                                              \
     do {                                                                                 \
-        if ((a).timers && threadIdx.x == 0) (a).timers[(size_t)blockIdx.x * 8 + (k)] = (v); \
+        if ((a).timers && threadIdx.x == 0) (a).timers[(size_t)blockIdx.x * 16 + (k)] = (v); \
     } while (0)
 #else
 #define PHASE_MARK(a, k) do {} while (0)
@@ -185,27 +187,49 @@ __device__ __forceinline__ uint32_t bin_cutoff(uint32_t tau) {
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63u); }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t t = __shfl_up(x, (unsigned)d, 64);
-        if (lane >= d) x += t;
-    }
-    return x;
+// Inclusive wave64 prefix sum with DPP row shifts and row broadcasts (no LDS
+// round trips).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xf, 0xf, false); // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xf, 0xf, false); // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xf, 0xf, false); // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x118, 0xf, 0xf, false); // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x142, 0xa, 0xf, false); // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x143, 0xc, 0xf, false); // row_bcast:31
+    return v;
+}
+
+// Wave64 OR / AND of a value; the result is valid in lane 63.
+__device__ __forceinline__ uint32_t wave_or_to63(uint32_t v) {
+    v |= __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0u, v, 0x118, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0u, v, 0x142, 0xa, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0u, v, 0x143, 0xc, 0xf, false);
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_and_to63(uint32_t v) {
+    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x111, 0xf, 0xf, false);
+    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x112, 0xf, 0xf, false);
+    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x114, 0xf, 0xf, false);
+    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x118, 0xf, 0xf, false);
+    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x142, 0xa, 0xf, false);
+    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x143, 0xc, 0xf, false);
+    return v;
 }
 
 // Wave-aggregated append: every lane of the wave must call it.  Returns the
 // slot of this lane's item (meaningful only where pred is true).
 __device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t *ctr) {
     const uint64_t m = __ballot(pred);
-    const uint32_t cnt = (uint32_t)__popcll(m);
+    if (m == 0) return 0;
     const uint32_t pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
     uint32_t base = 0;
-    if (lane_id() == 0 && cnt) base = atomicAdd(ctr, cnt);
-    base = __shfl(base, 0, 64);
-    return base + pre;
+    if (lane_id() == 0) base = atomicAdd(ctr, (uint32_t)__popcll(m));
+    return __builtin_amdgcn_readfirstlane(base) + pre;
 }
 
 // Wave-aggregated append for a ballot mask already computed by the caller:
@@ -230,19 +254,19 @@ struct Find {
 // level 2: 32 lanes scan the owner's bins.  Lane 0 writes *out.  A target of 0
 // or above the total yields bin = 2048.
 __device__ __forceinline__ void wave_find_level2(const uint32_t *hist, uint32_t incl, uint32_t tot,
-                                 uint32_t total, uint32_t k, Find *out) {
+                                                 uint32_t total, uint32_t k, Find *out) {
     const int lane = lane_id();
     if (k == 0 || k > total) {
         if (lane == 0) { out->bin = kBins; out->below = total; out->eq = 0; }
         return;
     }
     const int owner = __ffsll((unsigned long long)__ballot(incl >= k)) - 1;
-    const uint32_t base = __shfl(incl - tot, owner, 64);
+    const uint32_t base = __builtin_amdgcn_readlane(incl - tot, owner);
     const uint32_t v = (lane < 32) ? hist[owner * 32 + lane] : 0u;
     const uint32_t incl2 = wave_incl_scan(v);
     const int l2 = __ffsll((unsigned long long)__ballot(lane < 32 && base + incl2 >= k)) - 1;
-    const uint32_t below = base + __shfl(incl2 - v, l2, 64);
-    const uint32_t eq = __shfl(v, l2, 64);
+    const uint32_t below = base + __builtin_amdgcn_readlane(incl2 - v, l2);
+    const uint32_t eq = __builtin_amdgcn_readlane(v, l2);
     if (lane == 0) { out->bin = (uint32_t)(owner * 32 + l2); out->below = below; out->eq = eq; }
 }
 
@@ -256,7 +280,7 @@ __device__ __forceinline__ void wave_find(const uint32_t *hist, uint32_t k0, uin
         tot += t.x + t.y + t.z + t.w;
     }
     const uint32_t incl = wave_incl_scan(tot);
-    const uint32_t total = __shfl(incl, 63, 64);
+    const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
     wave_find_level2(hist, incl, tot, total, k0, &out[0]);
     if (nk > 1) wave_find_level2(hist, incl, tot, total, k1, &out[1]);
 }
@@ -265,9 +289,11 @@ __device__ __forceinline__ void wave_find(const uint32_t *hist, uint32_t k0, uin
 
 struct alignas(16) Smem {
     uint32_t hist[kBins];
+    uint32_t hist2[kBins]; // refinement alternates between hist and hist2
     uint32_t ci[kFront]; // frontier indices (row-relative)
     uint32_t ck[kFront]; // frontier keys: FP32 bits after Phase 2, kappa32 after compaction
     uint32_t wcnt[kWaves]; // Phase 2 hits per wave (exact, may exceed kWaveCap)
+    uint32_t red[2][4];    // refinement: OR (lo, hi) and AND (lo, hi) of live keys
     Find find[2];
     uint32_t cnt;       // C(tau1), or the append counter of the current pass
     uint32_t cnt0;      // C(tau0)
@@ -515,46 +541,6 @@ __device__ __forceinline__ uint32_t count_range(Smem &sm, const float *scores, i
     return sm.cnt0;
 }
 
-// Rewrites the stored entries as a contiguous frontier of (index, kappa32)
-// holding only the values with ascending key >= kmin: A(tau0) for a certified
-// proposal (kmin = cut0), A(tau1) for the band (kmin = cut1).  The source is
-// either the per-wave regions of Phase 2 (segmented) or [0, n) (contiguous),
-// both holding FP32 bits.  Entries are staged in registers, so the rewrite
-// is in place.  Returns the new count; ends with a barrier.
-__device__ __forceinline__ uint32_t compact_frontier(Smem &sm, bool segmented, uint32_t n,
-                                                     uint32_t kmin) {
-    constexpr int kPer = kFront / kBlock;
-    const int tid = threadIdx.x;
-    uint32_t ri[kPer], rb[kPer];
-    bool rv[kPer];
-#pragma unroll
-    for (int j = 0; j < kPer; j++) {
-        const uint32_t t = (uint32_t)(j * kBlock + tid);
-        bool v;
-        if (segmented) {
-            const uint32_t w = t / kWaveStride;
-            v = (t - w * kWaveStride) < min(sm.wcnt[w], (uint32_t)kWaveCap);
-        } else {
-            v = t < n;
-        }
-        ri[j] = v ? sm.ci[t] : 0u;
-        rb[j] = v ? sm.ck[t] : 0u;
-        rv[j] = v && asc_key(rb[j]) >= kmin;
-    }
-    if (tid == 0) sm.next = 0;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kPer; j++) {
-        const uint32_t q = wave_append(rv[j], &sm.next);
-        if (rv[j]) {
-            sm.ci[q] = ri[j];
-            sm.ck[q] = ~asc_key(rb[j]);
-        }
-    }
-    __syncthreads();
-    return sm.next;
-}
-
 // ----------------------------------------------------------- outputs ----
 
 __device__ __forceinline__ void emit(const KArgs a, int r, uint32_t pos, uint32_t idx,
@@ -588,66 +574,166 @@ __device__ __forceinline__ void write_error_row(const KArgs a, int r) {
 
 // ------------------------------------------------------- refinement ----
 
-// Phase 3 (Section 4.4): the LDS frontier sm.ci/ck[0..n) holds Q0 with quota
-// k; sm.opos outputs are already written.  Each round histograms one digit of
-// the composite key (kappa32: 11, 11, 10 bits; then the row index: 11, 11,
-// 10 bits), finds b = min{b : H(b) >= k}, commits the groups before b, keeps
-// group b, and stops once the kept group exactly fills the quota.  The kept
-// group is compacted in place, one 512-entry chunk at a time: a chunk is read
-// in full before any of its survivors is written, and survivors only ever go
-// below the end of the chunks already read.  Entry and exit with all threads
-// converged and sm.hist cleared.
-__device__ __forceinline__ void refine(const KArgs a, Smem &sm, int r, uint32_t n, uint32_t k, int64_t L) {
+// Phase 3 (Section 4.4).  The frontier Q0 (quota k; sm.opos outputs already
+// written) is read once into registers, kPer entries per thread, from either
+// the per-wave regions of Phase 2 (`segmented`) or [0, n) of sm.ci/ck, as
+// FP32 bits filtered by ascending key >= kmin (`raw`) or as kappa32 keys.
+// The entries are ordered by the composite key z = (kappa32 << 32) | index
+// (ties broken toward the lowest index).  Each round histograms an 11-bit
+// digit of z over the live entries, finds b = min{b : H(b) >= k}
+// (eq:method:digit-boundary), commits the groups before b
+// (eq:method:committed-group), keeps group b (eq:method:refine-recurrence)
+// and stops once the kept group exactly fills the quota.  The paper's digits
+// are fixed 11/11/10-bit fields of kappa32; here each round takes the 11 bits
+// just below the highest bit position at which the live keys still differ
+// (all live keys agree above it), which selects the same set in fewer rounds
+// and spreads the histogram over more bins.  Entries never move: each thread
+// keeps a live mask.  Entry and exit with all threads converged and sm.hist
+// cleared.
+constexpr int kPer = kFront / kBlock;
+
+__device__ __forceinline__ uint64_t zkey(uint32_t kappa, uint32_t idx) {
+    return ((uint64_t)kappa << 32) | idx;
+}
+
+// Block-wide OR and AND of the live composite keys into sm.red[par][0..3]
+// (written by one lane per wave; the caller's next barrier publishes them).
+__device__ __forceinline__ void reduce_live(Smem &sm, int par, const uint32_t *ri,
+                                            const uint32_t *rk, uint32_t live) {
+    uint32_t olo = 0, ohi = 0, alo = ~0u, ahi = ~0u;
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        if (live & (1u << j)) {
+            olo |= ri[j]; ohi |= rk[j];
+            alo &= ri[j]; ahi &= rk[j];
+        }
+    }
+    olo = wave_or_to63(olo);
+    ohi = wave_or_to63(ohi);
+    alo = wave_and_to63(alo);
+    ahi = wave_and_to63(ahi);
+    if (lane_id() == 63) {
+        atomicOr(&sm.red[par][0], olo);
+        atomicOr(&sm.red[par][1], ohi);
+        atomicAnd(&sm.red[par][2], alo);
+        atomicAnd(&sm.red[par][3], ahi);
+    }
+}
+
+// Lowest bit of the 11-bit digit window: just below the highest differing bit.
+__device__ __forceinline__ uint32_t window_shift(const Smem &sm, int par) {
+    const uint64_t o = ((uint64_t)sm.red[par][1] << 32) | sm.red[par][0];
+    const uint64_t n = ((uint64_t)sm.red[par][3] << 32) | sm.red[par][2];
+    const uint64_t diff = o ^ n;
+    const int h = diff ? 63 - __clzll((long long)diff) : 0;
+    return h >= 10 ? (uint32_t)(h - 10) : 0u;
+}
+
+__device__ __forceinline__ void reset_red(Smem &sm, int par) {
+    if (threadIdx.x < 4) sm.red[par][threadIdx.x] = threadIdx.x < 2 ? 0u : ~0u;
+}
+
+__device__ __forceinline__ void refine(const KArgs a, Smem &sm, int r, bool segmented, uint32_t n,
+                                       bool raw, uint32_t kmin, uint32_t n_live, uint32_t k,
+                                       int64_t L) {
+    (void)L;
     const int tid = threadIdx.x;
-    for (int j = 0; j < 6 && k > 0 && n > k; j++) {
-        if (j == 3 && L <= (1 << 21)) continue;              // index bits 21..31 are 0
-        if (j == 4 && L <= (1 << 10)) continue;              // index bits 10..20 are 0
-        const bool on_idx = j >= 3;
-        const int jj = on_idx ? j - 3 : j;
-        const uint32_t shift = jj == 0 ? 21u : (jj == 1 ? 10u : 0u);
-        const uint32_t mask = jj == 2 ? 0x3FFu : 0x7FFu;
-        for (uint32_t t = tid; t < n; t += kBlock)
-            atomicAdd(&sm.hist[((on_idx ? sm.ci[t] : sm.ck[t]) >> shift) & mask], 1u);
+    uint32_t ri[kPer], rk[kPer];
+    uint32_t live = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const uint32_t t = (uint32_t)(j * kBlock + tid);
+        bool v;
+        if (segmented) {
+            const uint32_t w = t / kWaveStride;
+            v = (t - w * kWaveStride) < min(sm.wcnt[w], (uint32_t)kWaveCap);
+        } else {
+            v = t < n;
+        }
+        ri[j] = v ? sm.ci[t] : 0u;
+        const uint32_t word = v ? sm.ck[t] : 0u;
+        if (raw) {
+            rk[j] = ~asc_key(word);
+            v = v && asc_key(word) >= kmin;
+        } else {
+            rk[j] = word;
+        }
+        live |= (v ? 1u : 0u) << j;
+    }
+    PHASE_WORD(a, 14, n_live);
+    int rounds_run = 0;
+    uint32_t done = 0; // committed entries (written out after the last round)
+    if (k > 0 && n_live > k) {
+        // sm.red[0] and sm.red[1] were reset by the caller before its barrier
+        reduce_live(sm, 0, ri, rk, live);
         __syncthreads();
-        if (tid < 64) wave_find(sm.hist, k, 0, 1, sm.find);
+    }
+    // Round t histograms into H[t & 1], finds into sm.find[t & 1] and
+    // reduces its survivors into sm.red[(t + 1) & 1]; each buffer of the
+    // other parity is reset while this round histograms (its last readers
+    // are behind this round's first barrier... of the previous round).
+    while (k > 0 && n_live > k) {
+        const int par = rounds_run & 1;
+        const uint32_t shift = window_shift(sm, par);
+        uint32_t *H = par ? sm.hist2 : sm.hist;
+        uint32_t *Hn = par ? sm.hist : sm.hist2;
+        {
+            uint4 *h4 = reinterpret_cast<uint4 *>(Hn);
+            for (int i = tid; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < kPer; j++)
+            if (live & (1u << j))
+                atomicAdd(&H[(uint32_t)(zkey(rk[j], ri[j]) >> shift) & 0x7FFu], 1u);
         __syncthreads();
-        const Find f = sm.find[0];
+        if (tid < 64) wave_find(H, k, 0, 1, &sm.find[par]);
+        reset_red(sm, par ^ 1);
+        __syncthreads();
+        const Find f = sm.find[par];
         const uint32_t need = k - f.below;                   // > 0 and <= f.eq
         const bool take_all = (f.eq == need);
-        clear_hist(sm);
-        if (tid == 0) sm.next = 0;
-        __syncthreads();
-        for (uint32_t c0 = 0; c0 < n; c0 += kBlock) {
-            const uint32_t t = c0 + tid;
-            const bool live = t < n;
-            uint32_t idx = 0, key = 0;
-            if (live) { idx = sm.ci[t]; key = sm.ck[t]; }
-            const uint32_t d = ((on_idx ? idx : key) >> shift) & mask;
-            const bool commit = live && (d < f.bin || (take_all && d == f.bin));
-            const bool keep = live && !take_all && d == f.bin;
-            const uint32_t op = wave_append(commit, &sm.opos);
-            if (commit) emit(a, r, op, idx, key);
-            __syncthreads();                                 // chunk fully read
-            const uint32_t kp = wave_append(keep, &sm.next);
-            if (keep) { sm.ci[kp] = idx; sm.ck[kp] = key; }
+        uint32_t keep = 0;
+#pragma unroll
+        for (int j = 0; j < kPer; j++) {
+            const bool lv = (live >> j) & 1u;
+            const uint32_t d = (uint32_t)(zkey(rk[j], ri[j]) >> shift) & 0x7FFu;
+            done |= ((lv && (d < f.bin || (take_all && d == f.bin))) ? 1u : 0u) << j;
+            keep |= ((lv && !take_all && d == f.bin) ? 1u : 0u) << j;
         }
-        __syncthreads();
-        if (take_all) { k = 0; n = 0; break; }
-        n = f.eq;
-        k = need;
-    }
-    if (k > 0) {
-        // n == k: commit the whole remaining frontier.
-        for (uint32_t t0 = 0; t0 < n; t0 += kBlock) {
-            const uint32_t t = t0 + tid;
-            const bool live = t < n;
-            uint32_t idx = 0, key = 0;
-            if (live) { idx = sm.ci[t]; key = sm.ck[t]; }
-            const uint32_t op = wave_append(live, &sm.opos);
-            if (live) emit(a, r, op, idx, key);
+        live = keep;
+        n_live = take_all ? 0u : f.eq;
+        k = take_all ? 0u : need;
+        if (rounds_run < 3) PHASE_MARK(a, 10 + rounds_run);
+        rounds_run++;
+        if (k > 0 && n_live > k) {
+            reduce_live(sm, par ^ 1, ri, rk, live);
+            __syncthreads();
         }
-        __syncthreads();
     }
+    // both histogram buffers back to zero for the next user of sm.hist
+    __syncthreads();
+    clear_hist(sm);
+    {
+        uint4 *h4 = reinterpret_cast<uint4 *>(sm.hist2);
+        for (int i = tid; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
+    }
+    PHASE_WORD(a, 15, (uint64_t)rounds_run);
+    if (k > 0) done |= live; // every live entry is in: n_live == k
+    // Output: one LDS atomic per wave places this thread's committed entries
+    // (no global store inside the rounds, so no barrier waits on one).
+    const uint32_t mine = (uint32_t)__popc(done);
+    const uint32_t incl = wave_incl_scan(mine);
+    const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+    uint32_t base = 0;
+    if (total) {
+        if (lane_id() == 63) base = atomicAdd(&sm.opos, total);
+        base = __builtin_amdgcn_readlane(base, 63);
+    }
+    uint32_t op = base + incl - mine;
+#pragma unroll
+    for (int j = 0; j < kPer; j++)
+        if (done & (1u << j)) emit(a, r, op++, ri[j], rk[j]);
+    __syncthreads();
 }
 
 // ------------------------------------------------------ exact routes ----
@@ -845,6 +931,7 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     clear_hist(sm);
     if (threadIdx.x == 0) sm.opos = 0;
     __syncthreads();
+    PHASE_MARK(a, 8);
     if (!sampled) {
         route = TOPK_ROUTE_EXACT_UNSAMPLED;
     } else if (C0 >= K && C0 <= cap) {
@@ -863,15 +950,20 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     } else {
         route = TOPK_ROUTE_EXACT_OVERFLOW;
     }
+    // Frontier of the certified tail: A(tau0), or A(tau1) for the band, read
+    // from the Phase 2 entries (FP32 bits filtered by kmin) or, when those
+    // are incomplete, re-collected from the row as kappa32 keys.
+    bool f_seg = segmented, f_raw = true;
+    uint32_t f_n = nstored;
     if (n_ref) {
-        // Frontier of the certified tail: A(tau0), or A(tau1) for the band.
-        if (!incomplete) {
-            compact_frontier(sm, segmented, nstored, kmin);
-        } else {
+        if (incomplete) {
             if (threadIdx.x == 0) sm.cnt = 0;
             __syncthreads();
             collect_range<false>(sm, a.scores, off, 0, (int32_t)L, kmin, 0xFFFFFFFFu, true, cap);
             __syncthreads();
+            f_seg = false;
+            f_raw = false;
+            f_n = n_ref;
         }
         nq = (int32_t)n_ref;
     }
@@ -883,12 +975,22 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
         k_ref = K - f.below;
         if (f.eq <= cap) {
             n_ref = f.eq;
+            f_seg = false;
+            f_raw = false;
+            f_n = f.eq;
         } else {
             route |= TOPK_ROUTE_REREAD_FLAG;
             reread_select(a, sm, r, off, L, f.bin, k_ref);
         }
     }
-    if (n_ref) refine(a, sm, r, n_ref, k_ref, L);
+    PHASE_MARK(a, 9);
+    if (n_ref) {
+        reset_red(sm, 0);
+        reset_red(sm, 1);
+        __syncthreads();
+        refine(a, sm, r, f_seg, f_n, f_raw, kmin, n_ref, k_ref, L);
+    }
+    PHASE_MARK(a, 13);
     if (threadIdx.x == 0) {
         atomicAdd(&a.hdr->stats[route & 7u], 1u);
         if (route & TOPK_ROUTE_REREAD_FLAG) atomicAdd(&a.hdr->stats[kStatReread], 1u);
