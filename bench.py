@@ -79,6 +79,79 @@ def cpu_baseline(wl, budget_s: float, threads: int):
             "us_per_call": round(el / reps * 1e6, 1)}
 
 
+def copy_calibration(mib: int, steps: int, warmup: int):
+    """A plain device-to-device copy of a known size (the runtime's copy
+    kernel), timed with HIP events.  Run under rocprofv3 --pmc, its FETCH_SIZE
+    and WRITE_SIZE readings calibrate the same counters taken on the Top-K
+    kernel: each should read `bytes` per dispatch."""
+    import torch
+
+    dev = torch.device("cuda", 0)
+    n = (mib << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.zeros_like(src)
+    for _ in range(warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    ev1.record()
+    ev1.synchronize()
+    us = ev0.elapsed_time(ev1) * 1e3 / max(1, steps)
+    print(json.dumps({"calibration": "device-to-device copy", "bytes": 4 * n,
+                      "us_per_copy": round(us, 3),
+                      "read_plus_write_GBs": round(8.0 * n / (us * 1e-6) / 1e9, 1)}), flush=True)
+
+
+def _pmc_mean_kib(csv_path: str, kernel_substr: str, counter: str, min_grid: int = 0):
+    import csv
+
+    vals = []
+    with open(csv_path, newline="") as fh:
+        for row in csv.DictReader(fh):
+            if (kernel_substr in row["Kernel_Name"] and row["Counter_Name"] == counter
+                    and int(row["Grid_Size"]) >= min_grid):
+                vals.append(float(row["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"no {counter} rows for {kernel_substr!r} in {csv_path}")
+    return sum(vals) / len(vals), len(vals)
+
+
+def traffic_summary(paths, config: int, copy_mib: int, out_path: str):
+    """Turns four rocprofv3 --pmc counter CSVs (kernel FETCH_SIZE, kernel
+    WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE) into HBM bytes per launch of
+    the Top-K kernel, each counter scaled by copy_bytes / copy_reading."""
+    kf, kw, cf, cw = paths
+    copy_bytes = copy_mib << 20
+    f_kib, nf = _pmc_mean_kib(kf, "topk_ragged_kernel", "FETCH_SIZE")
+    w_kib, nw = _pmc_mean_kib(kw, "topk_ragged_kernel", "WRITE_SIZE")
+    cf_kib, _ = _pmc_mean_kib(cf, "copyBuffer", "FETCH_SIZE")
+    cw_kib, _ = _pmc_mean_kib(cw, "copyBuffer", "WRITE_SIZE")
+    sf = copy_bytes / (cf_kib * 1024.0)
+    sw = copy_bytes / (cw_kib * 1024.0)
+    wl = make_workload(config)
+    fetch = f_kib * 1024.0 * sf
+    write = w_kib * 1024.0 * sw
+    out = {"config": config, "kernel": "topk_ragged_kernel",
+           "kernel_source_sha256_16": kernel_source_hash(),
+           "fetch_kib_per_dispatch": round(f_kib, 1), "write_kib_per_dispatch": round(w_kib, 1),
+           "dispatches": [nf, nw],
+           "copy_bytes": copy_bytes, "copy_fetch_kib": round(cf_kib, 1),
+           "copy_write_kib": round(cw_kib, 1),
+           "fetch_scale": round(sf, 4), "write_scale": round(sw, 4),
+           "hbm_fetch_bytes_per_launch": round(fetch), "hbm_write_bytes_per_launch": round(write),
+           "hbm_bytes_per_launch": round(fetch + write),
+           "algorithmic_bytes_per_launch": 4 * wl.total_len,
+           "traffic_over_algorithmic": round((fetch + write) / (4.0 * wl.total_len), 4)}
+    with open(out_path, "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -89,13 +162,27 @@ def main():
     ap.add_argument("--calls-per-graph", type=int, default=0, help="0 = number of rotated copies")
     ap.add_argument("--no-rotate", action="store_true", help="reuse one copy (cache-resident input)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time; 0 = skip")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only time a plain device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--traffic-summary", nargs=4, metavar="CSV",
+                    help="kernel FETCH_SIZE, kernel WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE "
+                         "counter CSVs from rocprofv3 --pmc; writes the traffic file and exits")
+    ap.add_argument("--copy-mib", type=int, default=1024, help="size of the calibration copy")
     args = ap.parse_args()
+
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary, args.config, args.copy_mib, TRAFFIC_FILE)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(rows shard independently across GPUs; see DESIGN.md).", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, max(1, args.steps), args.warmup)
+        return
 
     import torch
 
