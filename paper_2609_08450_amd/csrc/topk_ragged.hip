@@ -27,6 +27,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <climits>
+#include <cstdlib>
 #include <type_traits>
 
 #include "../../include/topk_ragged.h"
@@ -44,6 +45,7 @@ static_assert(kCap <= kFront, "policy capacity must fit the storage");
 constexpr int kVec = 8;                     // 16-byte loads per thread per chunk
 static_assert(kVec * 4 <= 64, "per-thread element masks are 64-bit");
 static_assert(kFront % kBlock == 0 && kFront % kWaves == 0, "frontier layout");
+constexpr int kPer = kFront / kBlock;       // frontier slots per thread
 constexpr int kChunkVecs = kBlock * kVec;   // 16-byte vectors per chunk
 constexpr int kMaxSplit = 64;               // most segments per row
 constexpr int kSegMin = 8192;               // shortest segment, elements
@@ -58,17 +60,16 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 // Per-row state of a split row.  Row r of a split call owns the workspace
 // block at kHeaderBytes + r * kRowBlockBytes: this state, padded to 256
 // bytes, then kFront candidate indices and kFront candidate FP32 bit patterns
-// (the segments' A(tau1) entries, concatenated).
+// (the segments' A(tau1) entries, concatenated).  Every field and entry is
+// written and read with agent-scope atomic accesses (see the arrive step).
 struct RowState {
-    uint32_t flag;       // 1 once cut0/cut1/taus are published by segment 0
-    uint32_t cut0;       // ascending-key endpoint of tau0
-    uint32_t cut1;       // ascending-key endpoint of tau1
-    uint32_t taus;       // tau0 | tau1 << 16
+    uint32_t taus;       // segment 0's tau0 | tau1 << 16 | 1 << 31 once known
     uint32_t arrive;     // segments done with Phase 2
     uint32_t count1;     // C(tau1) of the row (exact)
     uint32_t count0;     // C(tau0) of the row (exact)
     uint32_t stored;     // entries reserved in the candidate buffer
     uint32_t incomplete; // a segment could not keep all of its A(tau1)
+    uint32_t amax;       // largest ascending key among the stored entries
 };
 
 // Workspace header (first kHeaderBytes of the workspace).
@@ -95,6 +96,7 @@ struct KArgs {
     int32_t n_rows;
     int32_t K;
     int32_t pmax;
+    int32_t seg_items; // split rows: aim for about this many (row, segment) items
     int32_t s_log2;
     int32_t q0, q1;
     int32_t l_samp_min;
@@ -114,11 +116,11 @@ struct KArgs {
 #define PHASE_MARK(a, k)                                                                 \
     do {                                                                                 \
         if ((a).timers && threadIdx.x == 0)                                              \
-            (a).timers[(size_t)blockIdx.x * 16 + (k)] = wall_clock64();                   \
+            (a).timers[(size_t)blockIdx.x * 32 + (k)] = wall_clock64();                   \
     } while (0)
 #define PHASE_WORD(a, k, v)                                                              \
     do {                                                                                 \
-        if ((a).timers && threadIdx.x == 0) (a).timers[(size_t)blockIdx.x * 16 + (k)] = (v); \
+        if ((a).timers && threadIdx.x == 0) (a).timers[(size_t)blockIdx.x * 32 + (k)] = (v); \
     } while (0)
 #else
 #define PHASE_MARK(a, k) do {} while (0)
@@ -220,6 +222,27 @@ __device__ __forceinline__ uint32_t wave_and_to63(uint32_t v) {
     return v;
 }
 
+// Wave64 minimum / maximum; the result is valid in lane 63.
+__device__ __forceinline__ uint32_t wave_min_to63(uint32_t v) {
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x111, 0xf, 0xf, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x112, 0xf, 0xf, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x114, 0xf, 0xf, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x118, 0xf, 0xf, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x142, 0xa, 0xf, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x143, 0xc, 0xf, false));
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_max_to63(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x111, 0xf, 0xf, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x112, 0xf, 0xf, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x114, 0xf, 0xf, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x118, 0xf, 0xf, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x142, 0xa, 0xf, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x143, 0xc, 0xf, false));
+    return v;
+}
+
 // Wave-aggregated append: every lane of the wave must call it.  Returns the
 // slot of this lane's item (meaningful only where pred is true).
 __device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t *ctr) {
@@ -293,16 +316,20 @@ struct alignas(16) Smem {
     uint32_t ci[kFront]; // frontier indices (row-relative)
     uint32_t ck[kFront]; // frontier keys: FP32 bits after Phase 2, kappa32 after compaction
     uint32_t wcnt[kWaves]; // Phase 2 hits per wave (exact, may exceed kWaveCap)
-    uint32_t red[2][4];    // refinement: OR (lo, hi) and AND (lo, hi) of live keys
+    uint32_t red[4];       // refinement: min/max kappa32, min/max index of the live keys
+    uint32_t coarse[2][64]; // refinement: 32-bin group sums of hist / hist2
     Find find[2];
     uint32_t cnt;       // C(tau1), or the append counter of the current pass
     uint32_t cnt0;      // C(tau0)
     uint32_t incomplete;
     uint32_t opos;      // outputs written for the current row
-    uint32_t next;      // compaction counter in refinement
+    uint32_t wc[kWaves];  // refinement: entries committed by each wave in a pass
+    uint32_t wk[kWaves];  // refinement: entries kept by each wave in a pass
     uint32_t cut0, cut1, tau0, tau1;
     uint32_t flag;
     uint32_t base;
+    int64_t lsum[kWaves]; // per-wave partial sums of the row lengths
+    uint32_t amax;        // largest ascending key among the stored entries
 };
 
 __device__ __forceinline__ void clear_hist(Smem &sm) {
@@ -338,13 +365,12 @@ struct NoPrologue {
 // consumed, the next one is in flight.  Loads are unconditional -- lanes and
 // chunks past the end re-read the last vector of the range (one cache line per
 // wave), masked by the window test -- so the in-order load counter lets each
-// consume wait for its own chunk only.  prologue() runs once, by every thread:
-// before the first issue when it loads from memory itself (its loads would
-// otherwise queue behind the chunk), else with the first chunk in flight.
+// consume wait for its own chunk only.  prologue() runs once, by every thread,
+// with the first chunk in flight (loads it waits for must have been issued
+// before the call, or they would queue behind the chunk).
 template <bool kNT, class F, class Pro = NoPrologue>
 __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int32_t beg,
-                                           int32_t end, F &&fn, Pro &&prologue = Pro(),
-                                           bool prologue_first = false) {
+                                           int32_t end, F &&fn, Pro &&prologue = Pro()) {
     if (beg >= end) {
         prologue();
         return;
@@ -378,9 +404,8 @@ __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int
         const bool edge = ibase + cb * 4 < beg || ibase + (cb + mv * kBlock) * 4 > end;
         fn(src, i0, beg, end, edge, mv);
     };
-    if (prologue_first) prologue();
     issue(xa, 0);
-    if (!prologue_first) prologue();
+    prologue();
     for (int32_t c = 0; c < nch; c += 2) {
         issue(xb, c + 1);
         consume(xa, c);
@@ -445,8 +470,7 @@ __device__ __forceinline__ void collect_range(Smem &sm, const float *scores, int
 // set).  The endpoints are read from sm after prologue() has run.
 template <class Pro>
 __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, int64_t off,
-                                               int32_t beg, int32_t end, bool prologue_first,
-                                               Pro &&prologue) {
+                                               int32_t beg, int32_t end, Pro &&prologue) {
     const int w = threadIdx.x >> 6;
     uint32_t cur = 0; // wave-uniform: hits so far
     stream_row<true>(
@@ -492,7 +516,7 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
                 else run(std::false_type{}, std::false_type{});
             }
         },
-        prologue, prologue_first);
+        prologue);
     if ((threadIdx.x & 63) == 0) {
         sm.wcnt[w] = cur;
         atomicAdd(&sm.cnt, cur);
@@ -500,23 +524,24 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
     }
 }
 
-// C(tau0) from the stored entries of Phase 2 (all of A(tau1) when complete).
-// Ends with a barrier.
-__device__ __forceinline__ uint32_t count_tail(Smem &sm, bool segmented, uint32_t n,
-                                               uint32_t kmin) {
-    uint32_t c = 0;
-    for (uint32_t t = threadIdx.x; t < (uint32_t)kFront; t += kBlock) {
-        bool v;
-        if (segmented) {
-            const uint32_t w = t / kWaveStride;
-            v = (t - w * kWaveStride) < min(sm.wcnt[w], (uint32_t)kWaveCap);
-        } else {
-            v = t < n;
-        }
-        c += (v && asc_key(sm.ck[t]) >= kmin) ? 1u : 0u;
+// C(tau0) from the stored entries of Phase 2 (all of A(tau1) when complete,
+// in the per-wave regions), and into sm.amax the largest ascending key
+// stored.  sm.cnt0 and sm.amax must be zero on entry.  Ends with a barrier.
+__device__ __forceinline__ uint32_t count_tail(Smem &sm, uint32_t kmin) {
+    const uint32_t w = threadIdx.x >> 6;
+    const uint32_t beg = w * kWaveStride, end = beg + min(sm.wcnt[w], (uint32_t)kWaveCap);
+    uint32_t c = 0, mx = 0;
+    for (uint32_t e = beg + (uint32_t)lane_id(); e < end; e += 64) {
+        const uint32_t u = asc_key(sm.ck[e]);
+        c += u >= kmin ? 1u : 0u;
+        mx = max(mx, u);
     }
     c = wave_incl_scan(c);
-    if ((threadIdx.x & 63) == 63 && c) atomicAdd(&sm.cnt0, c);
+    mx = wave_max_to63(mx);
+    if ((threadIdx.x & 63) == 63) {
+        if (c) atomicAdd(&sm.cnt0, c);
+        atomicMax(&sm.amax, mx);
+    }
     __syncthreads();
     return sm.cnt0;
 }
@@ -575,164 +600,341 @@ __device__ __forceinline__ void write_error_row(const KArgs a, int r) {
 // ------------------------------------------------------- refinement ----
 
 // Phase 3 (Section 4.4).  The frontier Q0 (quota k; sm.opos outputs already
-// written) is read once into registers, kPer entries per thread, from either
-// the per-wave regions of Phase 2 (`segmented`) or [0, n) of sm.ci/ck, as
-// FP32 bits filtered by ascending key >= kmin (`raw`) or as kappa32 keys.
-// The entries are ordered by the composite key z = (kappa32 << 32) | index
-// (ties broken toward the lowest index).  Each round histograms an 11-bit
-// digit of z over the live entries, finds b = min{b : H(b) >= k}
-// (eq:method:digit-boundary), commits the groups before b
-// (eq:method:committed-group), keeps group b (eq:method:refine-recurrence)
-// and stops once the kept group exactly fills the quota.  The paper's digits
-// are fixed 11/11/10-bit fields of kappa32; here each round takes the 11 bits
-// just below the highest bit position at which the live keys still differ
-// (all live keys agree above it), which selects the same set in fewer rounds
-// and spreads the histogram over more bins.  Entries never move: each thread
-// keeps a live mask.  Entry and exit with all threads converged and sm.hist
-// cleared.
-constexpr int kPer = kFront / kBlock;
-
+// written) stays in sm.ci/ck, as FP32 bits filtered by ascending key >= kmin
+// (`raw`) or as kappa32 keys, in per-wave ranges: the wave regions of Phase
+// 2 (`segmented`) or eighths of [0, n).  Entries are ordered by the composite
+// key z = (kappa32 << 32) | index (ties broken toward the lowest index).
+// Each round histograms an 11-bit digit of z over the live entries, finds
+// b = min{b : H(b) >= k} (eq:method:digit-boundary), commits the groups
+// before b (eq:method:committed-group), keeps group b
+// (eq:method:refine-recurrence) and stops once the kept group exactly fills
+// the quota.  The paper's digits are fixed 11/11/10-bit fields of kappa32.
+// Here the first digit is taken from the live keys' range instead:
+// d(z) = (z - lo) >> w, with lo the smallest live key and w the smallest
+// shift that maps the range into 2048 bins; every later round takes the next
+// 11 bits of the same offset key inside the kept bin.  Bins are contiguous
+// key ranges in key order, as radix digits are, so the selected set is the
+// same, in fewer rounds: a frontier between 1.9 and 5.0 spans four exponent
+// values, which fixed digits would split into a handful of bins.  The live
+// entries of a round are exactly those whose key lies in the kept key range
+// [lo, hi], so no per-entry state is kept.  Once at most kSmall entries are
+// live, the rest is settled by ranking them against each other.  Every pass
+// is a loop of each wave over its own range.
 __device__ __forceinline__ uint64_t zkey(uint32_t kappa, uint32_t idx) {
     return ((uint64_t)kappa << 32) | idx;
 }
 
-// Block-wide OR and AND of the live composite keys into sm.red[par][0..3]
-// (written by one lane per wave; the caller's next barrier publishes them).
-__device__ __forceinline__ void reduce_live(Smem &sm, int par, const uint32_t *ri,
-                                            const uint32_t *rk, uint32_t live) {
-    uint32_t olo = 0, ohi = 0, alo = ~0u, ahi = ~0u;
-#pragma unroll
-    for (int j = 0; j < kPer; j++) {
-        if (live & (1u << j)) {
-            olo |= ri[j]; ohi |= rk[j];
-            alo &= ri[j]; ahi &= rk[j];
+__device__ __forceinline__ void reset_range(Smem &sm) {
+    if (threadIdx.x < 4) sm.red[threadIdx.x] = (threadIdx.x & 1) ? 0u : ~0u;
+}
+
+constexpr uint32_t kSmall = 512;
+
+// The live key range of a round, [lo, hi] over composite keys, digit
+// d(z) = (z - lo) >> w.  When the range covers whole kappa32 values and the
+// digit lies above the index bits (w >= 32), keys and digits are taken from
+// kappa32 alone (klo, khi, wf = w - 32): the common case, with half the work.
+struct Window {
+    uint64_t lo, hi;
+    uint32_t w;
+    bool fast;
+    uint32_t klo, kspan, wf;
+};
+
+__device__ __forceinline__ Window make_window(uint64_t lo, uint64_t hi, uint32_t w) {
+    Window v;
+    v.lo = lo; v.hi = hi; v.w = w;
+    v.fast = w >= 32 && (uint32_t)lo == 0u && (uint32_t)hi == 0xFFFFFFFFu;
+    v.klo = (uint32_t)(lo >> 32);
+    v.kspan = (uint32_t)(hi >> 32) - v.klo;
+    v.wf = v.fast ? w - 32 : 0u;
+    return v;
+}
+
+// Frontier entry e of the refinement: its kappa32 and FP32 bits.
+struct Ent {
+    uint32_t kk, bits;
+};
+
+__device__ __forceinline__ Ent read_ent(const Smem &sm, uint32_t e, bool raw) {
+    const uint32_t word = sm.ck[e];
+    Ent x;
+    x.kk = raw ? ~asc_key(word) : word;
+    x.bits = raw ? word : bits_from_asc(~word);
+    return x;
+}
+
+// Per-entry classes against the window and boundary bin b: live, below b,
+// in b.  kFast: 32-bit keys (index bits not part of the digit).
+template <bool kFast>
+struct Classifier {
+    Window v;
+    uint32_t cb, ce; // fast: below iff t < cb, in b iff cb <= t <= ce (t = kk - klo)
+    uint32_t b;
+    __device__ __forceinline__ Classifier(const Window &win, uint32_t bin) : v(win), b(bin) {
+        cb = bin << win.wf;
+        const uint32_t top = cb + (((uint32_t)1 << win.wf) - 1u);
+        ce = min(top, win.kspan);
+    }
+    __device__ __forceinline__ bool live(const Smem &sm, uint32_t e, const Ent &x) const {
+        if constexpr (kFast) return x.kk - v.klo <= v.kspan;
+        const uint64_t z = zkey(x.kk, sm.ci[e]);
+        return z >= v.lo && z <= v.hi;
+    }
+    __device__ __forceinline__ uint32_t digit(const Smem &sm, uint32_t e, const Ent &x) const {
+        if constexpr (kFast) return (x.kk - v.klo) >> v.wf;
+        return (uint32_t)((zkey(x.kk, sm.ci[e]) - v.lo) >> v.w);
+    }
+    // below b / in b, both implying live
+    __device__ __forceinline__ void cls(const Smem &sm, uint32_t e, const Ent &x, bool &below,
+                                        bool &inb) const {
+        if constexpr (kFast) {
+            const uint32_t t = x.kk - v.klo;
+            below = t < cb && t <= v.kspan;
+            inb = t >= cb && t <= ce;
+        } else {
+            const uint64_t z = zkey(x.kk, sm.ci[e]);
+            const bool lv = z >= v.lo && z <= v.hi;
+            const uint32_t d = lv ? (uint32_t)((z - v.lo) >> v.w) : 0u;
+            below = lv && d < b;
+            inb = lv && d == b;
         }
     }
-    olo = wave_or_to63(olo);
-    ohi = wave_or_to63(ohi);
-    alo = wave_and_to63(alo);
-    ahi = wave_and_to63(ahi);
-    if (lane_id() == 63) {
-        atomicOr(&sm.red[par][0], olo);
-        atomicOr(&sm.red[par][1], ohi);
-        atomicAnd(&sm.red[par][2], alo);
-        atomicAnd(&sm.red[par][3], ahi);
+};
+
+// Writes output slot pos of this refinement (entry e, class known).
+__device__ __forceinline__ void put_out(const KArgs a, int64_t out0, uint32_t pos, uint32_t idx,
+                                        uint32_t bits) {
+    a.out_idx[out0 + pos] = (int32_t)idx;
+    a.out_val[out0 + pos] = __builtin_bit_cast(float, bits);
+}
+
+// Ranks the nk keys of the LDS table zs against each other and writes the k
+// lowest to output slots placed + rank.  Wave v ranks table entries
+// [64 v, 64 v + 64) against the whole table, 64 keys at a time read across
+// lanes.  Needs the table complete (caller's barrier).
+__device__ __forceinline__ void rank_small(const KArgs a, int64_t out0, const uint64_t *zs,
+                                           uint32_t nk, uint32_t k, uint32_t placed) {
+    const uint32_t w8 = threadIdx.x >> 6, lane = (uint32_t)lane_id();
+    if (64 * w8 >= nk) return;
+    const uint32_t i = 64 * w8 + lane;
+    // keys are below 2^64 - 1 (indices are below 2^31): ~0 pads never count
+    const uint64_t z = i < nk ? zs[i] : ~0ull;
+    uint32_t rank = 0;
+    for (uint32_t c = 0; c < nk; c += 64) {
+        const uint64_t y = (c + lane < nk) ? zs[c + lane] : ~0ull;
+        const uint32_t ylo = (uint32_t)y, yhi = (uint32_t)(y >> 32);
+        const uint32_t m = min(64u, nk - c);
+        for (uint32_t l = 0; l < m; l++) {
+            const uint64_t v = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(yhi, l) << 32) |
+                               (uint32_t)__builtin_amdgcn_readlane(ylo, l);
+            rank += (v < z) ? 1u : 0u;
+        }
+    }
+    if (i < nk && rank < k)
+        put_out(a, out0, placed + rank, (uint32_t)z, bits_from_asc(~(uint32_t)(z >> 32)));
+}
+
+// Per-wave exclusive prefix and total of sm.wc / sm.wk (after a barrier).
+__device__ __forceinline__ void wave_bases(const Smem &sm, uint32_t &cbase, uint32_t &kbase,
+                                           uint32_t &ctotal) {
+    const uint32_t w8 = threadIdx.x >> 6;
+    cbase = 0; kbase = 0; ctotal = 0;
+#pragma unroll
+    for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
+        const uint32_t c = sm.wc[v], q = sm.wk[v];
+        if (v < w8) { cbase += c; kbase += q; }
+        ctotal += c;
     }
 }
 
-// Lowest bit of the 11-bit digit window: just below the highest differing bit.
-__device__ __forceinline__ uint32_t window_shift(const Smem &sm, int par) {
-    const uint64_t o = ((uint64_t)sm.red[par][1] << 32) | sm.red[par][0];
-    const uint64_t n = ((uint64_t)sm.red[par][3] << 32) | sm.red[par][2];
-    const uint64_t diff = o ^ n;
-    const int h = diff ? 63 - __clzll((long long)diff) : 0;
-    return h >= 10 ? (uint32_t)(h - 10) : 0u;
-}
-
-__device__ __forceinline__ void reset_red(Smem &sm, int par) {
-    if (threadIdx.x < 4) sm.red[par][threadIdx.x] = threadIdx.x < 2 ? 0u : ~0u;
+// One refinement round over the live entries of window win (quota k):
+// histogram, boundary bin, count and place.  Returns true when the row is
+// complete; otherwise win, n_live and k describe the next round.
+template <bool kFast>
+__device__ __forceinline__ bool refine_round(const KArgs a, Smem &sm, uint32_t beg, uint32_t end,
+                                             bool raw, int64_t out0, uint32_t &placed,
+                                             Window &win, uint32_t &n_live, uint32_t &k,
+                                             int par) {
+    const int tid = threadIdx.x;
+    const uint32_t lane = (uint32_t)lane_id(), w8 = (uint32_t)tid >> 6;
+    uint32_t *H = par ? sm.hist2 : sm.hist;
+    uint32_t *C = sm.coarse[par];
+    {
+        uint4 *h4 = reinterpret_cast<uint4 *>(par ? sm.hist : sm.hist2);
+        for (int i = tid; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
+        if (tid < 64) sm.coarse[par ^ 1][tid] = 0u;
+    }
+    {
+        const Classifier<kFast> q(win, 0u);
+        for (uint32_t e = beg + lane; e < end; e += 64) {
+            const Ent x = read_ent(sm, e, raw);
+            if (q.live(sm, e, x)) {
+                const uint32_t d = q.digit(sm, e, x);
+                atomicAdd(&H[d], 1u);
+                atomicAdd(&C[d >> 5], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    if (tid < 64) {
+        // two levels: 64 coarse groups of 32 bins, then the owner's bins
+        const uint32_t c = C[tid];
+        const uint32_t incl = wave_incl_scan(c);
+        const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+        wave_find_level2(H, incl, c, total, k, &sm.find[par]);
+    }
+    __syncthreads();
+    const Find f = sm.find[par];
+    const uint32_t need = k - f.below; // > 0 and <= f.eq
+    const bool take_all = f.eq == need;
+    const bool rank_next = !take_all && f.eq <= kSmall;
+    const Classifier<kFast> q(win, f.bin);
+    // count pass: entries committed (below b, or up to b with take_all) and
+    // kept for ranking, per wave
+    uint32_t cw = 0, kw = 0;
+    for (uint32_t e = beg + lane; e < end; e += 64) {
+        const Ent x = read_ent(sm, e, raw);
+        bool below, inb;
+        q.cls(sm, e, x, below, inb);
+        cw += (uint32_t)__popcll(__ballot(below || (take_all && inb)));
+        kw += (uint32_t)__popcll(__ballot(rank_next && inb));
+    }
+    if (lane == 0) { sm.wc[w8] = cw; sm.wk[w8] = kw; }
+    __syncthreads();
+    uint32_t cbase, kbase, committed;
+    wave_bases(sm, cbase, kbase, committed);
+    cbase += placed;
+    // place pass: committed entries to consecutive output slots of each
+    // wave, kept ones to the rank table
+    uint64_t *zs = reinterpret_cast<uint64_t *>(par ? sm.hist : sm.hist2);
+    for (uint32_t e = beg + lane; e < end; e += 64) {
+        const Ent x = read_ent(sm, e, raw);
+        bool below, inb;
+        q.cls(sm, e, x, below, inb);
+        const bool commit = below || (take_all && inb);
+        const bool keep = rank_next && inb;
+        const uint64_t mc = __ballot(commit);
+        const uint64_t mk = __ballot(keep);
+        if (commit || keep) {
+            const uint32_t idx = sm.ci[e];
+            if (commit)
+                put_out(a, out0, cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
+                                         __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u)),
+                        idx, x.bits);
+            else
+                zs[kbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32),
+                                __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u))] = zkey(x.kk, idx);
+        }
+        cbase += (uint32_t)__popcll(mc);
+        kbase += (uint32_t)__popcll(mk);
+    }
+    placed += committed;
+    if (take_all) return true;
+    k -= committed;
+    if (rank_next) {
+        __syncthreads();
+        rank_small(a, out0, zs, f.eq, k, placed);
+        return true;
+    }
+    // next round inside the kept bin: the 11 bits below w
+    n_live = f.eq;
+    const uint64_t blo = win.lo + ((uint64_t)f.bin << win.w);
+    win = make_window(blo, blo + (((uint64_t)1 << win.w) - 1), win.w > 11 ? win.w - 11 : 0u);
+    __syncthreads(); // sm.wc is rewritten by the next count pass
+    return false;
 }
 
 __device__ __forceinline__ void refine(const KArgs a, Smem &sm, int r, bool segmented, uint32_t n,
-                                       bool raw, uint32_t kmin, uint32_t n_live, uint32_t k,
-                                       int64_t L) {
-    (void)L;
+                                       bool raw, uint32_t amin, uint32_t amax, uint32_t n_live,
+                                       uint32_t k) {
     const int tid = threadIdx.x;
-    uint32_t ri[kPer], rk[kPer];
-    uint32_t live = 0;
-#pragma unroll
-    for (int j = 0; j < kPer; j++) {
-        const uint32_t t = (uint32_t)(j * kBlock + tid);
-        bool v;
-        if (segmented) {
-            const uint32_t w = t / kWaveStride;
-            v = (t - w * kWaveStride) < min(sm.wcnt[w], (uint32_t)kWaveCap);
-        } else {
-            v = t < n;
-        }
-        ri[j] = v ? sm.ci[t] : 0u;
-        const uint32_t word = v ? sm.ck[t] : 0u;
-        if (raw) {
-            rk[j] = ~asc_key(word);
-            v = v && asc_key(word) >= kmin;
-        } else {
-            rk[j] = word;
-        }
-        live |= (v ? 1u : 0u) << j;
+    const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
+    // this wave's entries: [beg, end)
+    uint32_t beg, end;
+    if (segmented) {
+        beg = w8 * kWaveStride;
+        end = beg + min(sm.wcnt[w8], (uint32_t)kWaveCap);
+    } else {
+        const uint32_t per = (n + kWaves - 1) / kWaves;
+        beg = min(n, w8 * per);
+        end = min(n, beg + per);
     }
     PHASE_WORD(a, 14, n_live);
-    int rounds_run = 0;
-    uint32_t done = 0; // committed entries (written out after the last round)
-    if (k > 0 && n_live > k) {
-        // sm.red[0] and sm.red[1] were reset by the caller before its barrier
-        reduce_live(sm, 0, ri, rk, live);
-        __syncthreads();
-    }
-    // Round t histograms into H[t & 1], finds into sm.find[t & 1] and
-    // reduces its survivors into sm.red[(t + 1) & 1]; each buffer of the
-    // other parity is reset while this round histograms (its last readers
-    // are behind this round's first barrier... of the previous round).
-    while (k > 0 && n_live > k) {
-        const int par = rounds_run & 1;
-        const uint32_t shift = window_shift(sm, par);
-        uint32_t *H = par ? sm.hist2 : sm.hist;
-        uint32_t *Hn = par ? sm.hist : sm.hist2;
-        {
-            uint4 *h4 = reinterpret_cast<uint4 *>(Hn);
-            for (int i = tid; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
+    const int64_t out0 = (int64_t)r * a.K + (a.K - k); // first output of this refinement
+    uint32_t placed = 0;                                // outputs written so far
+    // Live keys: ascending key in [amin, amax], i.e. kappa32 in [~amax, ~amin]
+    // (amax = 0: not known, measured by a pass over the entries).
+    uint32_t klo = amax ? ~amax : 0u, khi = ~amin;
+    if (k == 0) return;
+    if (n_live == k || n_live <= kSmall) {
+        // every live entry is in, or rank the live ones against each other
+        const bool all = n_live == k;
+        uint32_t cw = 0;
+        for (uint32_t e = beg + lane; e < end; e += 64) {
+            const Ent x = read_ent(sm, e, raw);
+            cw += (uint32_t)__popcll(__ballot(x.kk - klo <= khi - klo));
         }
-#pragma unroll
-        for (int j = 0; j < kPer; j++)
-            if (live & (1u << j))
-                atomicAdd(&H[(uint32_t)(zkey(rk[j], ri[j]) >> shift) & 0x7FFu], 1u);
+        if (lane == 0) { sm.wc[w8] = cw; sm.wk[w8] = cw; }
         __syncthreads();
-        if (tid < 64) wave_find(H, k, 0, 1, &sm.find[par]);
-        reset_red(sm, par ^ 1);
-        __syncthreads();
-        const Find f = sm.find[par];
-        const uint32_t need = k - f.below;                   // > 0 and <= f.eq
-        const bool take_all = (f.eq == need);
-        uint32_t keep = 0;
-#pragma unroll
-        for (int j = 0; j < kPer; j++) {
-            const bool lv = (live >> j) & 1u;
-            const uint32_t d = (uint32_t)(zkey(rk[j], ri[j]) >> shift) & 0x7FFu;
-            done |= ((lv && (d < f.bin || (take_all && d == f.bin))) ? 1u : 0u) << j;
-            keep |= ((lv && !take_all && d == f.bin) ? 1u : 0u) << j;
+        uint32_t base, kbase, total;
+        wave_bases(sm, base, kbase, total);
+        uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
+        for (uint32_t e = beg + lane; e < end; e += 64) {
+            const Ent x = read_ent(sm, e, raw);
+            const bool lv = x.kk - klo <= khi - klo;
+            const uint64_t m = __ballot(lv);
+            if (lv) {
+                const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+                if (all) put_out(a, out0, pos, sm.ci[e], x.bits);
+                else zs[pos] = zkey(x.kk, sm.ci[e]);
+            }
+            base += (uint32_t)__popcll(m);
         }
-        live = keep;
-        n_live = take_all ? 0u : f.eq;
-        k = take_all ? 0u : need;
-        if (rounds_run < 3) PHASE_MARK(a, 10 + rounds_run);
-        rounds_run++;
-        if (k > 0 && n_live > k) {
-            reduce_live(sm, par ^ 1, ri, rk, live);
+        if (!all) {
             __syncthreads();
+            rank_small(a, out0, zs, n_live, k, 0u);
+        }
+        __syncthreads();
+        return;
+    }
+    if (tid < 64) sm.coarse[0][tid] = 0u;
+    if (amax == 0u) {
+        // range pass: min/max kappa32 of the live entries
+        // (sm.red was reset by the caller before its barrier)
+        uint32_t kmn = ~0u, kmx = 0u;
+        for (uint32_t e = beg + lane; e < end; e += 64) {
+            const uint32_t kk = read_ent(sm, e, raw).kk;
+            if (kk <= khi) { kmn = min(kmn, kk); kmx = max(kmx, kk); }
+        }
+        kmn = wave_min_to63(kmn);
+        kmx = wave_max_to63(kmx);
+        if (lane == 63) {
+            atomicMin(&sm.red[0], kmn);
+            atomicMax(&sm.red[1], kmx);
         }
     }
-    // both histogram buffers back to zero for the next user of sm.hist
     __syncthreads();
-    clear_hist(sm);
-    {
-        uint4 *h4 = reinterpret_cast<uint4 *>(sm.hist2);
-        for (int i = tid; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
+    if (amax == 0u) {
+        klo = sm.red[0];
+        khi = sm.red[1];
+    }
+    // first window: all live keys, the smallest shift that fits 2048 bins
+    const uint64_t span0 = ((uint64_t)(khi - klo) << 32) | 0xFFFFFFFFull;
+    const int bits0 = 64 - __clzll((long long)span0);
+    Window win = make_window((uint64_t)klo << 32, ((uint64_t)khi << 32) | 0xFFFFFFFFull,
+                             bits0 > 11 ? (uint32_t)(bits0 - 11) : 0u);
+    int rounds_run = 0;
+    for (;;) {
+        const int par = rounds_run & 1;
+        const bool done = win.fast
+            ? refine_round<true>(a, sm, beg, end, raw, out0, placed, win, n_live, k, par)
+            : refine_round<false>(a, sm, beg, end, raw, out0, placed, win, n_live, k, par);
+        rounds_run++;
+        if (done) break;
     }
     PHASE_WORD(a, 15, (uint64_t)rounds_run);
-    if (k > 0) done |= live; // every live entry is in: n_live == k
-    // Output: one LDS atomic per wave places this thread's committed entries
-    // (no global store inside the rounds, so no barrier waits on one).
-    const uint32_t mine = (uint32_t)__popc(done);
-    const uint32_t incl = wave_incl_scan(mine);
-    const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
-    uint32_t base = 0;
-    if (total) {
-        if (lane_id() == 63) base = atomicAdd(&sm.opos, total);
-        base = __builtin_amdgcn_readlane(base, 63);
-    }
-    uint32_t op = base + incl - mine;
-#pragma unroll
-    for (int j = 0; j < kPer; j++)
-        if (done & (1u << j)) emit(a, r, op++, ri[j], rk[j]);
     __syncthreads();
 }
 
@@ -876,14 +1078,58 @@ __device__ __forceinline__ int64_t view_size(int64_t L, uint32_t a, int s_log2) 
 // Sample histogram over the view and the two boundaries (eq:method:sample-hist,
 // eq:method:primary-threshold); leaves tau0/tau1 and their endpoints in sm.
 // Ends with a barrier; the histogram is cleared again on exit.
-__device__ __forceinline__ void phase1(const KArgs a, Smem &sm, int r, const float *row, int64_t L) {
+// Sum of max(L_r, 0) over all rows of the call (every workgroup of a
+// splittable call computes it to size its row's segments).  Ends with a
+// barrier.
+__device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm) {
+    int64_t s = 0;
+    for (int t = threadIdx.x; t < a.n_rows; t += kBlock) s += (int64_t)max(a.lens[t], 0);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+    if (lane_id() == 0) sm.lsum[threadIdx.x >> 6] = s;
+    __syncthreads();
+    int64_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; w++) tot += sm.lsum[w];
+    return tot;
+}
+
+// Phase 1 in two halves.  phase1_issue loads the first kP1 view samples of
+// each thread into registers; it runs before the segment's first chunk is
+// issued so that waiting for the samples does not wait for the chunk.
+// phase1_finish histograms them (and the rest of the view, for views larger
+// than kP1 * kBlock), finds tau0 and tau1 and their FP32 endpoints
+// (eq:method:sample-hist, eq:method:primary-threshold) into sm.  Every
+// segment of a split row computes the same view (no cross-workgroup wait).
+// sm.hist must have been cleared before a barrier preceding phase1_finish.
+constexpr int kP1 = 16;
+
+__device__ __forceinline__ void phase1_issue(const KArgs a, int r, const float *row, int64_t L,
+                                             float (&xs)[kP1]) {
+    const uint32_t ph = view_phase(r, a.s_log2);
+    const int64_t nv = view_size(L, ph, a.s_log2);
+    const float *base = row + ph;
+#pragma unroll
+    for (int j = 0; j < kP1; j++) {
+        const int64_t t = threadIdx.x + (int64_t)j * kBlock;
+        xs[j] = 0.0f;
+        if (t < nv) xs[j] = base[t << a.s_log2];
+    }
+}
+
+__device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, const float *row,
+                                              int64_t L, const float (&xs)[kP1]) {
     const int tid = threadIdx.x;
     const uint32_t ph = view_phase(r, a.s_log2);
     const int64_t nv = view_size(L, ph, a.s_log2);
-    clear_hist(sm);
     __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kP1; j++) {
+        const int64_t t = tid + (int64_t)j * kBlock;
+        if (t < nv) atomicAdd(&sm.hist[coarse_bin(xs[j])], 1u);
+    }
     const float *base = row + ph;
-    int64_t t = tid;
+    int64_t t = tid + (int64_t)kP1 * kBlock;
     for (; t + 3 * kBlock < nv; t += 4 * kBlock) {
         const float x0 = base[(t) << a.s_log2];
         const float x1 = base[(t + kBlock) << a.s_log2];
@@ -955,6 +1201,8 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     // are incomplete, re-collected from the row as kappa32 keys.
     bool f_seg = segmented, f_raw = true;
     uint32_t f_n = nstored;
+    // ascending-key bounds of the frontier (f_amax = 0: not known)
+    uint32_t f_amin = kmin, f_amax = incomplete ? 0u : sm.amax;
     if (n_ref) {
         if (incomplete) {
             if (threadIdx.x == 0) sm.cnt = 0;
@@ -978,17 +1226,21 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
             f_seg = false;
             f_raw = false;
             f_n = f.eq;
+            // the frontier is coarse bin tau*: ascending keys from its
+            // endpoint up to below the endpoint of the bin above
+            f_amin = bin_cutoff(f.bin);
+            f_amax = f.bin > 0 ? bin_cutoff(f.bin - 1) - 1u : 0xFFFFFFFFu;
         } else {
             route |= TOPK_ROUTE_REREAD_FLAG;
             reread_select(a, sm, r, off, L, f.bin, k_ref);
         }
     }
     PHASE_MARK(a, 9);
+    if (f_amax != 0u && f_amax < f_amin) f_amax = 0u;
     if (n_ref) {
-        reset_red(sm, 0);
-        reset_red(sm, 1);
+        reset_range(sm);
         __syncthreads();
-        refine(a, sm, r, f_seg, f_n, f_raw, kmin, n_ref, k_ref, L);
+        refine(a, sm, r, f_seg, f_n, f_raw, f_amin, f_amax, n_ref, k_ref);
     }
     PHASE_MARK(a, 13);
     if (threadIdx.x == 0) {
@@ -1048,81 +1300,90 @@ topk_ragged_kernel(KArgs a) {
     const uint32_t ph = view_phase(r, a.s_log2);
     const int64_t nv = view_size(L, ph, a.s_log2);
     const bool sampled = L >= a.l_samp_min && nv >= a.q1;
+    if (!sampled && p > 0) return; // unsampled rows run whole on segment 0
 
-    // Segments of a sampled row: P0 = min(pmax, ceil(L / kSegMin)) pieces of
-    // equal length rounded up to 64 elements.  Unsampled rows run whole on
-    // segment 0.
-    int64_t P = 1, seg = L;
-    if (sampled) {
-        const int64_t P0 = min((int64_t)a.pmax, (L + kSegMin - 1) / kSegMin);
-        seg = (((L + P0 - 1) / P0) + 63) & ~(int64_t)63;
-        P = (L + seg - 1) / seg;
-    }
-    if (p >= P) return;
-    const bool split = P > 1;
     RowState *rs = reinterpret_cast<RowState *>(a.rows + (size_t)r * kRowBlockBytes);
     uint32_t *gi = reinterpret_cast<uint32_t *>(a.rows + (size_t)r * kRowBlockBytes +
                                                 kRowStateBytes);
     uint32_t *gk = gi + kFront;
     uint32_t C0 = 0, C1 = 0, nstored = 0;
-    bool incomplete = false, segmented = true;
+    bool incomplete = false, segmented = true, split = false;
 
     if (sampled) {
-        // Phase 1 runs while the first chunk of this segment is loading:
-        // segment 0 (or the only segment) builds the view; other segments
-        // wait for its published endpoints and rebuild the same view
-        // themselves if it does not arrive within the spin limit.
-        if (tid == 0) { sm.cnt = 0; sm.cnt0 = 0; sm.incomplete = 0; }
+        // A row has at most ceil(L / kSegMin) segments (see below).
+        if ((int64_t)p * kSegMin >= L) return;
+        clear_hist(sm);
+        if (tid == 0) { sm.cnt = 0; sm.cnt0 = 0; sm.incomplete = 0; sm.amax = 0; }
+        // Segment 0 reads the view; its loads go out first, the segment plan
+        // and the first chunk follow, and the view is histogrammed with that
+        // chunk in flight.
+        float xs[kP1];
+        if (p == 0) phase1_issue(a, r, row, L, xs);
+        // Segments: when rows may be split, a row is cut into P0 =
+        // min(pmax, ceil(L / target)) pieces of equal length rounded up to 64
+        // elements, target = max(kSegMin, sum(L) / items), so that the call
+        // has at most about seg_items work items.  P <= P0 <= ceil(L / kSegMin).
+        int64_t P = 1, seg = L;
+        if (a.pmax > 1) {
+            const int64_t total = block_total_length(a, sm);
+            const int64_t items = a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
+                                                             : (a.seg_items + 1) / 2;
+            const int64_t target = max((total + items - 1) / items, (int64_t)kSegMin);
+            const int64_t P0 = min((int64_t)a.pmax, (L + target - 1) / target);
+            seg = (((L + P0 - 1) / P0) + 63) & ~(int64_t)63;
+            P = (L + seg - 1) / seg;
+        }
+        if (p >= P) return;
+        split = P > 1;
         const int32_t beg = (int32_t)(p * seg);
         const int32_t end = (int32_t)min(L, p * seg + seg);
-        auto endpoints = [&]() {
-            bool own_view = !split || p == 0;
-            if (!own_view) {
+        // Phase 2 over this segment: certify against cut0 and keep A(tau1).
+        // The endpoints come from segment 0, which publishes tau0 and tau1 in
+        // one agent-scope atomic word (the endpoints follow from the bins);
+        // other segments poll for it with their first chunk in flight and
+        // build the view themselves if it does not come within the spin
+        // limit.  Segment 0 never waits for another segment, and every
+        // segment 0 is dispatched before any other segment, so the wait ends.
+        phase2_collect(sm, a.scores, off, beg, end, [&]() {
+            bool own = p == 0;
+            if (!own) {
                 if (tid == 0) {
-                    // Relaxed polls (an acquire per poll would invalidate this
-                    // XCD's L2 every time); one acquire once the flag is set.
-                    uint32_t f = 0;
+                    uint32_t v = 0;
                     for (int spin = 0; spin < kSpinLimit; spin++) {
-                        f = __hip_atomic_load(&rs->flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        if (f) break;
-                        __builtin_amdgcn_s_sleep(2);
+                        v = __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (v & 0x80000000u) break;
+                        __builtin_amdgcn_s_sleep(1);
                     }
-                    sm.flag = f;
-                    if (f) {
-                        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                        sm.cut0 = __hip_atomic_load(&rs->cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        sm.cut1 = __hip_atomic_load(&rs->cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        const uint32_t taus =
-                            __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        sm.tau0 = taus & 0xFFFFu;
-                        sm.tau1 = taus >> 16;
+                    if (v & 0x80000000u) {
+                        sm.flag = 1u;
+                        sm.tau0 = v & 0xFFFFu;
+                        sm.tau1 = (v >> 16) & 0x7FFFu;
+                        sm.cut0 = bin_cutoff(sm.tau0);
+                        sm.cut1 = bin_cutoff(sm.tau1);
                     } else {
+                        sm.flag = 0u;
                         atomicAdd(&a.hdr->stats[kStatWaitFallback], 1u);
                     }
                 }
                 __syncthreads();
-                own_view = sm.flag == 0;
+                if (sm.flag == 0u) {
+                    own = true;
+                    phase1_issue(a, r, row, L, xs);
+                }
             }
-            if (own_view) phase1(a, sm, r, row, L);
-            if (split && p == 0 && tid == 0) {
-                __hip_atomic_store(&rs->cut0, sm.cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&rs->cut1, sm.cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&rs->taus, sm.tau0 | (sm.tau1 << 16), __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&rs->flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-            }
+            if (own) phase1_finish(a, sm, r, row, L, xs);
+            if (split && p == 0 && tid == 0)
+                __hip_atomic_store(&rs->taus, sm.tau0 | (sm.tau1 << 16) | 0x80000000u,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             PHASE_MARK(a, 1);
-        };
-        // Phase 2 over this segment: certify against cut0 and keep A(tau1).
-        phase2_collect(sm, a.scores, off, beg, end, /*prologue_first=*/!split || p == 0,
-                       endpoints);
+        });
         __syncthreads();
         C1 = sm.cnt;
         incomplete = sm.incomplete != 0;
         // C(tau0): from the stored A(tau1) entries, or by re-reading this
         // segment when a wave region overflowed.
         C0 = incomplete ? count_range(sm, a.scores, off, beg, end, sm.cut0)
-                        : count_tail(sm, true, 0, sm.cut0);
+                        : count_tail(sm, sm.cut0);
         PHASE_MARK(a, 2);
         PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)P << 16) | ((uint64_t)r << 32));
 
@@ -1143,6 +1404,8 @@ topk_ragged_kernel(KArgs a) {
                 if (C0) __hip_atomic_fetch_add(&rs->count0, C0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (incomplete)
                     __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                else if (pre[kWaves])
+                    __hip_atomic_fetch_max(&rs->amax, sm.amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             __syncthreads();
             const uint32_t base = sm.base;
@@ -1150,49 +1413,66 @@ topk_ragged_kernel(KArgs a) {
                 const uint32_t w = t / kWaveStride, j = t - w * kWaveStride;
                 if (j < pre[w + 1] - pre[w]) {
                     const uint32_t d = base + pre[w] + j;
-                    if (d < (uint32_t)kFront) { gi[d] = sm.ci[t]; gk[d] = sm.ck[t]; }
+                    if (d < (uint32_t)kFront) {
+                        __hip_atomic_store(&gi[d], sm.ci[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&gk[d], sm.ck[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
                 }
             }
-            // Every wave waits for its own stores to reach L2; after the
-            // barrier one thread writes the L2 back for the other XCDs
-            // (agent-scope release) and arrives.
+            // Every value another workgroup reads (entries, counts, the
+            // arrival counter) is an agent-scope atomic access, which the
+            // hardware keeps coherent across the XCDs' L2 caches without a
+            // writeback or invalidate of the whole L2.  Each wave waits until
+            // its own accesses have completed; after the barrier all of them
+            // are visible device-wide, before the arrival is made.
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid == 0) {
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
                 const uint32_t old = __hip_atomic_fetch_add(&rs->arrive, 1u, __ATOMIC_RELAXED,
                                                             __HIP_MEMORY_SCOPE_AGENT);
-                const bool last = old == (uint32_t)(P - 1);
-                if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                sm.flag = last ? 2u : 0u;
+                sm.flag = (old == (uint32_t)(P - 1)) ? 2u : 0u;
             }
             __syncthreads();
             PHASE_MARK(a, 3);
             if (sm.flag != 2u) return;
 
-            // Finisher.  Segment 0 published the endpoints before arriving.
+            // Finisher (its sm.cut0, cut1, tau0, tau1 are the row's endpoints).
             if (tid == 0) {
                 sm.cnt = __hip_atomic_load(&rs->count1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.cnt0 = __hip_atomic_load(&rs->count0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.base = __hip_atomic_load(&rs->stored, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.incomplete = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                sm.cut0 = __hip_atomic_load(&rs->cut0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                sm.cut1 = __hip_atomic_load(&rs->cut1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                const uint32_t taus =
-                    __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                sm.tau0 = taus & 0xFFFFu;
-                sm.tau1 = taus >> 16;
+                sm.amax = __hip_atomic_load(&rs->amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             __syncthreads();
             C1 = sm.cnt;
             C0 = sm.cnt0;
             const uint32_t stored = sm.base;
             incomplete = sm.incomplete != 0 || stored > (uint32_t)kFront;
-            nstored = min(stored, (uint32_t)kFront);
+            nstored = incomplete ? 0u : stored;
             segmented = false;
-            for (uint32_t t = tid; t < nstored; t += kBlock) {
-                sm.ci[t] = gi[t];
-                sm.ck[t] = gk[t];
+            // The merged frontier into LDS: every load is issued before the
+            // first is used (one round trip), read as agent-scope atomics.
+            {
+                uint32_t vi[kPer], vk[kPer];
+#pragma unroll
+                for (int j = 0; j < kPer; j++) {
+                    const uint32_t t = (uint32_t)(j * kBlock + tid);
+                    vi[j] = 0u;
+                    vk[j] = 0u;
+                    if (t < nstored) {
+                        vi[j] = __hip_atomic_load(&gi[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        vk[j] = __hip_atomic_load(&gk[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < kPer; j++) {
+                    const uint32_t t = (uint32_t)(j * kBlock + tid);
+                    if (t < nstored) {
+                        sm.ci[t] = vi[j];
+                        sm.ck[t] = vk[j];
+                    }
+                }
             }
             __syncthreads();
             PHASE_MARK(a, 4);
@@ -1208,8 +1488,9 @@ topk_ragged_kernel(KArgs a) {
         __hip_atomic_store(&rs->count0, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&rs->stored, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&rs->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -1273,13 +1554,24 @@ uint32_t split_rows_for(int32_t max_rows, int cus) {
     return (uint32_t)((max_rows < lim) ? max_rows : lim);
 }
 
-// Segments per row: enough work items for about 8 workgroups per compute
-// unit, as a power of two in [1, kMaxSplit]; rows are split only when the
-// call has at most 4 x CUs rows.
+// Work-item target of a split call: 1.5 items per compute unit, below the
+// two workgroups per compute unit that can be resident (LDS bound), so that
+// every item of a call starts at once.
+int32_t plan_items(int cus) {
+#ifdef TOPK_PHASE_TIMERS
+    if (const char *e = getenv("TOPK_SEG_ITEMS")) return atoi(e);
+#endif
+    return (3 * cus) / 2;
+}
+
+// Most segments per row: a power of two in [1, kMaxSplit] with n_rows x pmax
+// at most twice the item target (the grid; workgroups beyond a row's actual
+// segment count exit at once).  Rows are split only when the call has at most
+// 4 x CUs rows.
 int32_t plan_pmax(int32_t n_rows, int cus) {
-    const int64_t target = 8ll * cus;
+    const int64_t lim = 2ll * plan_items(cus);
     int32_t p = 1;
-    while (p < kMaxSplit && (int64_t)(p * 2) * n_rows <= target) p *= 2;
+    while (p < kMaxSplit && (int64_t)(p * 2) * n_rows <= lim) p *= 2;
     return p;
 }
 
@@ -1375,6 +1667,7 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     a.n_rows = n_rows;
     a.K = K;
     a.pmax = pmax;
+    a.seg_items = plan_items(di.cus);
     a.s_log2 = pol.s_log2;
     a.q0 = sample_rank(K, pol.rho_num, pol.rho_den, pol.s_log2);
     a.q1 = sample_rank(K, pol.rho1_num, pol.rho1_den, pol.s_log2);
