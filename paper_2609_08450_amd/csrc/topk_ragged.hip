@@ -59,7 +59,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 // Per-row state of a split row.  Row r of a split call owns the workspace
 // block at kHeaderBytes + r * kRowBlockBytes: this state, padded to 256
-// bytes, then kFront candidate indices and kFront candidate FP32 bit patterns
+// bytes, then kFront candidates as 64-bit (index | FP32 bits << 32) words
 // (the segments' A(tau1) entries, concatenated).  Every field and entry is
 // written and read with agent-scope atomic accesses (see the arrive step).
 struct RowState {
@@ -1303,9 +1303,9 @@ topk_ragged_kernel(KArgs a) {
     if (!sampled && p > 0) return; // unsampled rows run whole on segment 0
 
     RowState *rs = reinterpret_cast<RowState *>(a.rows + (size_t)r * kRowBlockBytes);
-    uint32_t *gi = reinterpret_cast<uint32_t *>(a.rows + (size_t)r * kRowBlockBytes +
+    // the row's merged candidates: index | FP32 bits << 32
+    uint64_t *gc = reinterpret_cast<uint64_t *>(a.rows + (size_t)r * kRowBlockBytes +
                                                 kRowStateBytes);
-    uint32_t *gk = gi + kFront;
     uint32_t C0 = 0, C1 = 0, nstored = 0;
     bool incomplete = false, segmented = true, split = false;
 
@@ -1391,12 +1391,18 @@ topk_ragged_kernel(KArgs a) {
             // Publish this segment's entries and counts (eq:method:split-local),
             // then arrive; the last arrival merges them (eq:method:split-reduce)
             // and finishes the row.
-            uint32_t pre[kWaves + 1];
-            pre[0] = 0;
+            // this wave's stored entries, those of the waves before it, all
+            const uint32_t w8 = (uint32_t)tid >> 6;
+            uint32_t wcnt = 0, wpre = 0, nst = 0;
 #pragma unroll
-            for (int w = 0; w < kWaves; w++) pre[w + 1] = pre[w] + min(sm.wcnt[w], (uint32_t)kWaveCap);
+            for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
+                const uint32_t c = min(sm.wcnt[v], (uint32_t)kWaveCap);
+                wcnt = v == w8 ? c : wcnt;
+                wpre += v < w8 ? c : 0u;
+                nst += c;
+            }
             if (tid == 0) {
-                sm.base = pre[kWaves] ? __hip_atomic_fetch_add(&rs->stored, pre[kWaves],
+                sm.base = nst ? __hip_atomic_fetch_add(&rs->stored, nst,
                                                                __ATOMIC_RELAXED,
                                                                __HIP_MEMORY_SCOPE_AGENT)
                                       : 0u;
@@ -1404,20 +1410,18 @@ topk_ragged_kernel(KArgs a) {
                 if (C0) __hip_atomic_fetch_add(&rs->count0, C0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (incomplete)
                     __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                else if (pre[kWaves])
+                else if (nst)
                     __hip_atomic_fetch_max(&rs->amax, sm.amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             __syncthreads();
-            const uint32_t base = sm.base;
-            for (uint32_t t = tid; t < (uint32_t)kFront; t += kBlock) {
-                const uint32_t w = t / kWaveStride, j = t - w * kWaveStride;
-                if (j < pre[w + 1] - pre[w]) {
-                    const uint32_t d = base + pre[w] + j;
-                    if (d < (uint32_t)kFront) {
-                        __hip_atomic_store(&gi[d], sm.ci[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(&gk[d], sm.ck[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    }
-                }
+            // each wave copies its own region, consecutive slots
+            const uint32_t dst = sm.base + wpre;
+            for (uint32_t e = (uint32_t)lane_id(); e < wcnt; e += 64) {
+                const uint32_t d = dst + e;
+                const uint32_t t = w8 * kWaveStride + e;
+                if (d < (uint32_t)kFront)
+                    __hip_atomic_store(&gc[d], ((uint64_t)sm.ck[t] << 32) | sm.ci[t],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             // Every value another workgroup reads (entries, counts, the
             // arrival counter) is an agent-scope atomic access, which the
@@ -1458,12 +1462,11 @@ topk_ragged_kernel(KArgs a) {
 #pragma unroll
                 for (int j = 0; j < kPer; j++) {
                     const uint32_t t = (uint32_t)(j * kBlock + tid);
-                    vi[j] = 0u;
-                    vk[j] = 0u;
-                    if (t < nstored) {
-                        vi[j] = __hip_atomic_load(&gi[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        vk[j] = __hip_atomic_load(&gk[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    }
+                    uint64_t v = 0u;
+                    if (t < nstored)
+                        v = __hip_atomic_load(&gc[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    vi[j] = (uint32_t)v;
+                    vk[j] = (uint32_t)(v >> 32);
                 }
 #pragma unroll
                 for (int j = 0; j < kPer; j++) {
