@@ -323,6 +323,7 @@ struct alignas(16) Smem {
     uint32_t cnt0;      // C(tau0)
     uint32_t incomplete;
     uint32_t opos;      // outputs written for the current row
+    uint32_t knext;       // refinement: rank-table entries appended
     uint32_t wc[kWaves];  // refinement: entries committed by each wave in a pass
     uint32_t wk[kWaves];  // refinement: entries kept by each wave in a pass
     uint32_t cut0, cut1, tau0, tau1;
@@ -764,6 +765,7 @@ __device__ __forceinline__ bool refine_round(const KArgs a, Smem &sm, uint32_t b
         uint4 *h4 = reinterpret_cast<uint4 *>(par ? sm.hist : sm.hist2);
         for (int i = tid; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
         if (tid < 64) sm.coarse[par ^ 1][tid] = 0u;
+        if (tid == 0) sm.knext = 0u;
     }
     {
         const Classifier<kFast> q(win, 0u);
@@ -790,53 +792,89 @@ __device__ __forceinline__ bool refine_round(const KArgs a, Smem &sm, uint32_t b
     const bool take_all = f.eq == need;
     const bool rank_next = !take_all && f.eq <= kSmall;
     const Classifier<kFast> q(win, f.bin);
-    // count pass: entries committed (below b, or up to b with take_all) and
-    // kept for ranking, per wave
-    uint32_t cw = 0, kw = 0;
+    uint64_t *zs = reinterpret_cast<uint64_t *>(par ? sm.hist : sm.hist2);
+    if (take_all || rank_next) {
+        // Last round: each wave moves its committed entries (below b, or up
+        // to b with take_all) to the front of its own range, in place (an
+        // entry is only written over after it has been read), and appends
+        // the kept ones (bin b) to the rank table; then the committed
+        // entries go out in consecutive slots.
+        uint32_t cw = 0;
+        for (uint32_t e = beg + lane; e < end; e += 64) {
+            const Ent x = read_ent(sm, e, raw);
+            bool below, inb;
+            q.cls(sm, e, x, below, inb);
+            const bool commit = below || (take_all && inb);
+            const bool keep = rank_next && inb;
+            const uint64_t mc = __ballot(commit);
+            const uint64_t mk = __ballot(keep);
+            uint32_t kb = 0;
+            if (mk) {
+                const uint32_t first = (uint32_t)__ffsll((unsigned long long)mk) - 1u;
+                if (lane == first) kb = atomicAdd(&sm.knext, (uint32_t)__popcll(mk));
+                kb = __builtin_amdgcn_readlane(kb, first);
+            }
+            if (commit || keep) {
+                const uint32_t idx = sm.ci[e];
+                if (commit) {
+                    const uint32_t d = beg + cw + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
+                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u));
+                    sm.ci[d] = idx;
+                    sm.ck[d] = x.bits;
+                } else {
+                    zs[kb + __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32),
+                                __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u))] = zkey(x.kk, idx);
+                }
+            }
+            cw += (uint32_t)__popcll(mc);
+        }
+        if (lane == 0) sm.wc[w8] = cw;
+        __syncthreads();
+        // (lanes that left the loop early hold a partial cw: use the wave's)
+        uint32_t cbase = placed, committed = 0;
+#pragma unroll
+        for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
+            const uint32_t c = sm.wc[v];
+            cbase += v < w8 ? c : 0u;
+            committed += c;
+        }
+        const uint32_t ncw = sm.wc[w8];
+        for (uint32_t e = lane; e < ncw; e += 64)
+            put_out(a, out0, cbase + e, sm.ci[beg + e], sm.ck[beg + e]);
+        placed += committed;
+        if (take_all) return true;
+        k -= committed;
+        rank_small(a, out0, zs, f.eq, k, placed);
+        return true;
+    }
+    // Another round follows: count pass (entries below b per wave), then the
+    // place pass; the entries stay where they are.
+    uint32_t cw = 0;
     for (uint32_t e = beg + lane; e < end; e += 64) {
         const Ent x = read_ent(sm, e, raw);
         bool below, inb;
         q.cls(sm, e, x, below, inb);
-        cw += (uint32_t)__popcll(__ballot(below || (take_all && inb)));
-        kw += (uint32_t)__popcll(__ballot(rank_next && inb));
+        cw += (uint32_t)__popcll(__ballot(below));
     }
-    if (lane == 0) { sm.wc[w8] = cw; sm.wk[w8] = kw; }
+    if (lane == 0) { sm.wc[w8] = cw; sm.wk[w8] = 0u; }
     __syncthreads();
     uint32_t cbase, kbase, committed;
     wave_bases(sm, cbase, kbase, committed);
     cbase += placed;
-    // place pass: committed entries to consecutive output slots of each
-    // wave, kept ones to the rank table
-    uint64_t *zs = reinterpret_cast<uint64_t *>(par ? sm.hist : sm.hist2);
+    // place pass: committed entries to consecutive output slots of each wave
     for (uint32_t e = beg + lane; e < end; e += 64) {
         const Ent x = read_ent(sm, e, raw);
         bool below, inb;
         q.cls(sm, e, x, below, inb);
-        const bool commit = below || (take_all && inb);
-        const bool keep = rank_next && inb;
-        const uint64_t mc = __ballot(commit);
-        const uint64_t mk = __ballot(keep);
-        if (commit || keep) {
-            const uint32_t idx = sm.ci[e];
-            if (commit)
-                put_out(a, out0, cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
-                                         __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u)),
-                        idx, x.bits);
-            else
-                zs[kbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32),
-                                __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u))] = zkey(x.kk, idx);
-        }
+        const uint64_t mc = __ballot(below);
+        if (below)
+            put_out(a, out0, cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u)),
+                    sm.ci[e], x.bits);
         cbase += (uint32_t)__popcll(mc);
-        kbase += (uint32_t)__popcll(mk);
     }
     placed += committed;
-    if (take_all) return true;
     k -= committed;
-    if (rank_next) {
-        __syncthreads();
-        rank_small(a, out0, zs, f.eq, k, placed);
-        return true;
-    }
     // next round inside the kept bin: the 11 bits below w
     n_live = f.eq;
     const uint64_t blo = win.lo + ((uint64_t)f.bin << win.w);
