@@ -42,7 +42,7 @@ constexpr int kFront = 7168;                // LDS frontier storage (pairs)
 constexpr int kWaveCap = kFront / kWaves - 1; // Phase 2 storage per wave (+1 spill slot)
 constexpr int kWaveStride = kFront / kWaves;
 static_assert(kCap <= kFront, "policy capacity must fit the storage");
-constexpr int kVec = 8;                     // 16-byte loads per thread per chunk
+constexpr int kVec = 4;                     // 16-byte loads per thread per chunk
 static_assert(kVec * 4 <= 64, "per-thread element masks are 64-bit");
 static_assert(kFront % kBlock == 0 && kFront % kWaves == 0, "frontier layout");
 constexpr int kPer = kFront / kBlock;       // frontier slots per thread
