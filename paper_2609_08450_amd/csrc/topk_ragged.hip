@@ -19,10 +19,9 @@
 //                     (eq:method:split-reduce) and finishes the row.
 //
 // Keys: asc = order-preserving uint32 of the FP32 bits; the descending key
-// kappa32 = ~asc (Section 4.3) is what the frontier stores and what the
-// radix digits are taken from.  Ties at rank K are resolved by three more
-// radix digits over the row index, so the result is the K smallest composite
-// keys (kappa32, index): the lowest index wins among equal values.
+// kappa32 = ~asc (Section 4.3) is what the radix digits are taken from.  The
+// refinement orders the composite key (kappa32, index), so ties at rank K go
+// to the lowest index: the result is the K smallest composite keys.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -1113,9 +1112,6 @@ __device__ __forceinline__ int64_t view_size(int64_t L, uint32_t a, int s_log2) 
     return ((int64_t)a < L) ? (L - a + s - 1) >> s_log2 : 0;
 }
 
-// Sample histogram over the view and the two boundaries (eq:method:sample-hist,
-// eq:method:primary-threshold); leaves tau0/tau1 and their endpoints in sm.
-// Ends with a barrier; the histogram is cleared again on exit.
 // Sum of max(L_r, 0) over all rows of the call (every workgroup of a
 // splittable call computes it to size its row's segments).  Ends with a
 // barrier.
