@@ -161,6 +161,55 @@ def test_forced_routes(topk, name, kw):
         parity(topk, wl, policy=pol, where=f"{wl.name} / {name}")
 
 
+# --------------------------------------------------------- random sweep --
+
+def _random_workload(seed):
+    """Rows of random lengths (a third at most K) and value families (normal,
+    heavy ties, constant, -inf mix, decode mixture), seeded; n_rows alternates
+    between call sizes that split rows and ones that do not."""
+    rng = np.random.default_rng(2600 + seed)
+    K = int([1, 5, 64, 300, 1024, 2048, 777, 2048][seed % 8])
+    n_rows = int([7, 50, 700, 33, 500, 90, 400, 12][seed % 8])
+    rows = []
+    for r in range(n_rows):
+        if rng.random() < 0.3:
+            L = int(rng.integers(0, K + 1))
+        else:
+            L = int(np.exp(rng.uniform(np.log(K + 1), np.log(60000))))
+        fam = int(rng.integers(0, 5))
+        if fam == 0:
+            x = rng.standard_normal(L).astype(np.float32)
+        elif fam == 1:
+            x = np.round(rng.standard_normal(L) * 4).astype(np.float32)
+        elif fam == 2:
+            x = np.full(L, np.float32(rng.standard_normal()), np.float32)
+        elif fam == 3:
+            x = rng.standard_normal(L).astype(np.float32)
+            x[rng.random(L) < 0.4] = -np.inf
+        else:
+            x = W.decode_mixture_row(rng, L)
+        rows.append(x.astype(np.float32))
+    lens = np.array([r.size for r in rows], np.int32)
+    offs = np.zeros(n_rows, np.int64)
+    offs[1:] = np.cumsum(lens[:-1])
+    buf = np.concatenate(rows) if rows else np.zeros(0, np.float32)
+    return W.Workload(f"random{seed}", buf, offs, lens, K, "")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_sweep(topk, seed):
+    wl = _random_workload(seed)
+    pol = topk.default_policy()
+    choice = seed % 4
+    if choice == 1:
+        pol.cap = max(1, min(6144, 3 * wl.K // 2))
+    elif choice == 2:
+        pol.s_log2, pol.l_samp_min = 6, 0
+    elif choice == 3:
+        pol.rho_num, pol.rho_den, pol.rho1_num, pol.rho1_den = 1, 1, 5, 4
+    parity(topk, wl, policy=pol, where=f"random{seed}/policy{choice}")
+
+
 # ----------------------------------------------------------- edge cases --
 
 def _edge_workload():
