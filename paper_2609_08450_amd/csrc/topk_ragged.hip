@@ -335,6 +335,7 @@ struct alignas(16) Smem {
 __device__ __forceinline__ void clear_hist(Smem &sm) {
     uint4 *h4 = reinterpret_cast<uint4 *>(sm.hist);
     for (int i = threadIdx.x; i < kBins / 4; i += kBlock) h4[i] = make_uint4(0, 0, 0, 0);
+    if (threadIdx.x < 64) sm.coarse[0][threadIdx.x] = 0u;
 }
 
 // ---------------------------------------------------- row streaming ----
@@ -1151,16 +1152,25 @@ __device__ __forceinline__ void phase1_issue(const KArgs a, int r, const float *
     }
 }
 
+// pub (segment 0 of a split row): where tau0 | tau1 << 16 | 1 << 31 is
+// published for the other segments, as soon as it is known.
 __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, const float *row,
-                                              int64_t L, const float (&xs)[kP1]) {
+                                              int64_t L, const float (&xs)[kP1], uint32_t *pub) {
     const int tid = threadIdx.x;
     const uint32_t ph = view_phase(r, a.s_log2);
     const int64_t nv = view_size(L, ph, a.s_log2);
     __syncthreads();
+    PHASE_MARK(a, 17);
+    // bin counts, and their sums over groups of 32 bins for a two-level find
+    auto add = [&](float x) {
+        const uint32_t b = coarse_bin(x);
+        atomicAdd(&sm.hist[b], 1u);
+        atomicAdd(&sm.coarse[0][b >> 5], 1u);
+    };
 #pragma unroll
     for (int j = 0; j < kP1; j++) {
         const int64_t t = tid + (int64_t)j * kBlock;
-        if (t < nv) atomicAdd(&sm.hist[coarse_bin(xs[j])], 1u);
+        if (t < nv) add(xs[j]);
     }
     const float *base = row + ph;
     int64_t t = tid + (int64_t)kP1 * kBlock;
@@ -1169,23 +1179,33 @@ __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, co
         const float x1 = base[(t + kBlock) << a.s_log2];
         const float x2 = base[(t + 2 * kBlock) << a.s_log2];
         const float x3 = base[(t + 3 * kBlock) << a.s_log2];
-        atomicAdd(&sm.hist[coarse_bin(x0)], 1u);
-        atomicAdd(&sm.hist[coarse_bin(x1)], 1u);
-        atomicAdd(&sm.hist[coarse_bin(x2)], 1u);
-        atomicAdd(&sm.hist[coarse_bin(x3)], 1u);
+        add(x0);
+        add(x1);
+        add(x2);
+        add(x3);
     }
-    for (; t < nv; t += kBlock) atomicAdd(&sm.hist[coarse_bin(base[t << a.s_log2])], 1u);
+    for (; t < nv; t += kBlock) add(base[t << a.s_log2]);
     __syncthreads();
+    PHASE_MARK(a, 18);
     if (tid < 64) {
-        wave_find(sm.hist, (uint32_t)a.q0, (uint32_t)a.q1, 2, sm.find);
+        const uint32_t c = sm.coarse[0][tid];
+        const uint32_t incl = wave_incl_scan(c);
+        const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+        wave_find_level2(sm.hist, incl, c, total, (uint32_t)a.q0, &sm.find[0]);
+        wave_find_level2(sm.hist, incl, c, total, (uint32_t)a.q1, &sm.find[1]);
         if (tid == 0) {
-            sm.tau0 = sm.find[0].bin;
-            sm.tau1 = sm.find[1].bin;
-            sm.cut0 = bin_cutoff(sm.tau0);
-            sm.cut1 = bin_cutoff(sm.tau1);
+            const uint32_t t0 = sm.find[0].bin, t1 = sm.find[1].bin;
+            if (pub)
+                __hip_atomic_store(pub, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            sm.tau0 = t0;
+            sm.tau1 = t1;
+            sm.cut0 = bin_cutoff(t0);
+            sm.cut1 = bin_cutoff(t1);
         }
     }
     __syncthreads();
+    PHASE_MARK(a, 19);
     clear_hist(sm);
 }
 
@@ -1378,6 +1398,7 @@ topk_ragged_kernel(KArgs a) {
         // build the view themselves if it does not come within the spin
         // limit.  Segment 0 never waits for another segment, and every
         // segment 0 is dispatched before any other segment, so the wait ends.
+        PHASE_MARK(a, 16);
         phase2_collect(sm, a.scores, off, beg, end, [&]() {
             bool own = p == 0;
             if (!own) {
@@ -1388,6 +1409,7 @@ topk_ragged_kernel(KArgs a) {
                         if (v & 0x80000000u) break;
                         __builtin_amdgcn_s_sleep(1);
                     }
+                    PHASE_MARK(a, 20);
                     if (v & 0x80000000u) {
                         sm.flag = 1u;
                         sm.tau0 = v & 0xFFFFu;
@@ -1405,10 +1427,7 @@ topk_ragged_kernel(KArgs a) {
                     phase1_issue(a, r, row, L, xs);
                 }
             }
-            if (own) phase1_finish(a, sm, r, row, L, xs);
-            if (split && p == 0 && tid == 0)
-                __hip_atomic_store(&rs->taus, sm.tau0 | (sm.tau1 << 16) | 0x80000000u,
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (own) phase1_finish(a, sm, r, row, L, xs, split && p == 0 ? &rs->taus : nullptr);
             PHASE_MARK(a, 1);
         });
         __syncthreads();
