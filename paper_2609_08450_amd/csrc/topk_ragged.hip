@@ -1114,11 +1114,12 @@ __device__ __forceinline__ int64_t view_size(int64_t L, uint32_t a, int s_log2) 
 }
 
 // Sum of max(L_r, 0) over all rows of the call (every workgroup of a
-// splittable call computes it to size its row's segments).  Ends with a
-// barrier.
-__device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm) {
-    int64_t s = 0;
-    for (int t = threadIdx.x; t < a.n_rows; t += kBlock) s += (int64_t)max(a.lens[t], 0);
+// splittable call computes it to size its row's segments); len0 is this
+// thread's first term, lens[threadIdx.x] (0 past the last row), loaded
+// by the caller ahead of time.  Ends with a barrier.
+__device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm, int32_t len0) {
+    int64_t s = (int64_t)max(len0, 0);
+    for (int t = threadIdx.x + kBlock; t < a.n_rows; t += kBlock) s += (int64_t)max(a.lens[t], 0);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
     if (lane_id() == 0) sm.lsum[threadIdx.x >> 6] = s;
@@ -1187,22 +1188,24 @@ __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, co
     for (; t < nv; t += kBlock) add(base[t << a.s_log2]);
     __syncthreads();
     PHASE_MARK(a, 18);
-    if (tid < 64) {
-        const uint32_t c = sm.coarse[0][tid];
+    if (tid < 128) {
+        // wave 0 finds q0, wave 1 finds q1
+        const uint32_t c = sm.coarse[0][lane_id()];
         const uint32_t incl = wave_incl_scan(c);
         const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
-        wave_find_level2(sm.hist, incl, c, total, (uint32_t)a.q0, &sm.find[0]);
-        wave_find_level2(sm.hist, incl, c, total, (uint32_t)a.q1, &sm.find[1]);
-        if (tid == 0) {
-            const uint32_t t0 = sm.find[0].bin, t1 = sm.find[1].bin;
-            if (pub)
-                __hip_atomic_store(pub, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-            sm.tau0 = t0;
-            sm.tau1 = t1;
-            sm.cut0 = bin_cutoff(t0);
-            sm.cut1 = bin_cutoff(t1);
-        }
+        const int which = tid >> 6;
+        wave_find_level2(sm.hist, incl, c, total, (uint32_t)(which ? a.q1 : a.q0), &sm.find[which]);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t t0 = sm.find[0].bin, t1 = sm.find[1].bin;
+        if (pub)
+            __hip_atomic_store(pub, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        sm.tau0 = t0;
+        sm.tau1 = t1;
+        sm.cut0 = bin_cutoff(t0);
+        sm.cut1 = bin_cutoff(t1);
     }
     __syncthreads();
     PHASE_MARK(a, 19);
@@ -1309,7 +1312,143 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     }
 }
 
+// Finish of a split row certified on the primary or band route, straight
+// from the merged candidates in registers (vi, vk: index and FP32 bits of
+// slot j * kBlock + tid, valid below n): one digit round over the live key
+// range [~amax, ~cut] (fine histogram plus 32-bin group sums, two-level
+// find), committed entries written out from registers in consecutive slots
+// of each wave, the boundary bin ranked when it holds at most kSmall
+// entries.  Returns false, having written nothing, when the row needs the
+// general finish (other routes, unknown range, a tiny or narrow frontier, a
+// large boundary bin).  Needs sm.hist and sm.coarse[0] clear.
+__device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r, int64_t nv,
+                                                  uint32_t C0, uint32_t C1, uint32_t amax,
+                                                  uint32_t n, const uint32_t (&vi)[kPer],
+                                                  const uint32_t (&vk)[kPer]) {
+    const int tid = threadIdx.x;
+    const uint32_t lane = (uint32_t)lane_id(), w8 = (uint32_t)tid >> 6;
+    const uint32_t K = (uint32_t)a.K, cap = (uint32_t)a.cap;
+    uint32_t route, kmin, n_live;
+    if (C0 >= K && C0 <= cap) {
+        route = TOPK_ROUTE_PRIMARY; kmin = sm.cut0; n_live = C0;
+    } else if (C0 < K && C1 >= K && C1 <= cap) {
+        route = TOPK_ROUTE_BAND; kmin = sm.cut1; n_live = C1;
+    } else {
+        return false;
+    }
+    if (amax == 0u || amax < kmin || n_live <= kSmall || n_live == K) return false;
+    const uint32_t klo = ~amax, khi = ~kmin;
+    const uint64_t span0 = ((uint64_t)(khi - klo) << 32) | 0xFFFFFFFFull;
+    const int bits0 = 64 - __clzll((long long)span0);
+    const Window win = make_window((uint64_t)klo << 32, ((uint64_t)khi << 32) | 0xFFFFFFFFull,
+                                   bits0 > 11 ? (uint32_t)(bits0 - 11) : 0u);
+    if (!win.fast || win.kspan == 0xFFFFFFFFu) return false;
+    PHASE_MARK(a, 8);
+    // histogram of the live keys (sm.hist and its group sums are clear);
+    // tl[j]: key offset in the window, ~0 for a slot that is not live (the
+    // window spans less than 2^32 - 1 keys, so ~0 is no live offset)
+    uint32_t tl[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const uint32_t t = ~asc_key(vk[j]) - win.klo;
+        const bool lv = (uint32_t)(j * kBlock + tid) < n && t <= win.kspan;
+        tl[j] = lv ? t : 0xFFFFFFFFu;
+        if (lv) {
+            const uint32_t d = t >> win.wf;
+            atomicAdd(&sm.hist[d], 1u);
+            atomicAdd(&sm.coarse[0][d >> 5], 1u);
+        }
+    }
+    if (tid == 0) sm.knext = 0u;
+    __syncthreads();
+    PHASE_MARK(a, 9);
+    if (tid < 64) {
+        const uint32_t c = sm.coarse[0][tid];
+        const uint32_t incl = wave_incl_scan(c);
+        const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+        wave_find_level2(sm.hist, incl, c, total, K, &sm.find[0]);
+    }
+    __syncthreads();
+    PHASE_MARK(a, 10);
+    const Find f = sm.find[0];
+    const uint32_t need = K - f.below;
+    const bool take_all = f.eq == need;
+    if (f.bin >= (uint32_t)kBins || (!take_all && f.eq > kSmall)) return false;
+    // committed: offset below cend (bin b excluded, or included with
+    // take_all); kept: offset in [cb, ce] (bin b) when not take_all
+    const uint32_t cb = f.bin << win.wf;
+    const uint32_t ce = min(cb + (((uint32_t)1 << win.wf) - 1u), win.kspan);
+    const uint32_t cend = take_all ? ce + 1u : cb;
+    const uint32_t kw = ce - cb; // keep iff tl - cb <= kw (never for ~0: ce < ~0)
+    uint32_t cw = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; j++) cw += (uint32_t)__popcll(__ballot(tl[j] < cend));
+    if (lane == 0) sm.wc[w8] = cw;
+    __syncthreads();
+    PHASE_MARK(a, 11);
+    uint32_t cbase = 0;
+#pragma unroll
+    for (uint32_t v = 0; v < (uint32_t)kWaves; v++) cbase += v < w8 ? sm.wc[v] : 0u;
+    const int64_t out0 = (int64_t)r * a.K;
+    int32_t *oi = a.out_idx + out0;
+    float *ov = a.out_val + out0;
+    uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const bool commit = tl[j] < cend;
+        const uint64_t mc = __ballot(commit);
+        if (commit) {
+            const uint32_t pos = cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
+                                               __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u));
+            oi[pos] = (int32_t)vi[j];
+            ov[pos] = __builtin_bit_cast(float, vk[j]);
+        }
+        cbase += (uint32_t)__popcll(mc);
+        const bool keep = !take_all && tl[j] - cb <= kw;
+        const uint64_t mk = __ballot(keep);
+        if (mk) {
+            const uint32_t first = (uint32_t)__ffsll((unsigned long long)mk) - 1u;
+            uint32_t kb = 0;
+            if (lane == first) kb = atomicAdd(&sm.knext, (uint32_t)__popcll(mk));
+            kb = __builtin_amdgcn_readlane(kb, first);
+            if (keep)
+                zs[kb + __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32),
+                            __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u))] =
+                    zkey(~asc_key(vk[j]), vi[j]);
+        }
+    }
+    PHASE_MARK(a, 12);
+    PHASE_WORD(a, 30, f.eq);
+    if (!take_all) {
+        __syncthreads();
+        rank_small(a, out0, zs, f.eq, need, f.below);
+    }
+    PHASE_MARK(a, 13);
+    if (tid == 0) {
+        atomicAdd(&a.hdr->stats[route], 1u);
+        if (a.trace) {
+            int32_t *t = a.trace + (int64_t)r * TOPK_TRACE_WORDS;
+            t[0] = (int32_t)route; t[1] = (int32_t)nv;
+            t[2] = (int32_t)sm.tau0; t[3] = (int32_t)sm.tau1;
+            t[4] = (int32_t)C0; t[5] = route == TOPK_ROUTE_BAND ? (int32_t)C1 : -1;
+            t[6] = -1; t[7] = (int32_t)n_live;
+        }
+    }
+    return true;
+}
+
 // ----------------------------------------------------------- kernel ----
+
+// Leaves a split row's state zeroed for the next call (graph replays).
+__device__ __forceinline__ void reset_row_state(RowState *rs) {
+    __hip_atomic_store(&rs->count1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->count0, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->stored, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void
 topk_ragged_kernel(KArgs a) {
@@ -1318,17 +1457,25 @@ topk_ragged_kernel(KArgs a) {
     const int item = blockIdx.x;
     const int p = item / a.n_rows;
     const int r = item - p * a.n_rows;
-
-    const int64_t L = (int64_t)max(a.lens[r], 0);
+    // Every load the prologue needs goes out at once: the row's length and
+    // offset, the workspace header, and this thread's first term of the
+    // segment plan's length sum (used only when rows may be split).
+    const int32_t len_r = a.lens[r];
     const int64_t off = a.offs[r];
+    const int32_t len0_raw = a.lens[min(tid, a.n_rows - 1)];
+    const uint4 hw = *reinterpret_cast<const uint4 *>(a.hdr); // magic, split_rows, max_rows
+    // (keeps the compiler from sinking each load to its first use, which
+    // would make them four round trips instead of one)
+    asm volatile("" ::"s"(len_r), "s"(off), "s"(hw.x), "s"(hw.y), "s"(hw.z), "v"(len0_raw));
+    const int64_t L = (int64_t)max(len_r, 0);
     const float *row = a.scores + off;
     PHASE_MARK(a, 0);
     PHASE_WORD(a, 6, (uint64_t)__smid());
 
     // Workspace check: a split plan needs per-row state for every row.
-    const WsHeader *hdr = a.hdr;
-    if (hdr->magic != kMagic || (uint32_t)a.n_rows > hdr->max_rows ||
-        (a.pmax > 1 && (uint32_t)a.n_rows > hdr->split_rows)) {
+    const bool ws_bad = (hw.x != kMagic) | ((uint32_t)a.n_rows > hw.z) |
+                        ((a.pmax > 1) & ((uint32_t)a.n_rows > hw.y));
+    if (ws_bad) {
         if (p == 0) {
             write_error_row(a, r);
             if (tid == 0 && r == 0) atomicAdd(&a.hdr->stats[kStatErrors], 1u);
@@ -1379,7 +1526,7 @@ topk_ragged_kernel(KArgs a) {
         // has at most about seg_items work items.  P <= P0 <= ceil(L / kSegMin).
         int64_t P = 1, seg = L;
         if (a.pmax > 1) {
-            const int64_t total = block_total_length(a, sm);
+            const int64_t total = block_total_length(a, sm, tid < a.n_rows ? len0_raw : 0);
             const int64_t items = a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
                                                              : (a.seg_items + 1) / 2;
             const int64_t target = max((total + items - 1) / items, (int64_t)kSegMin);
@@ -1494,6 +1641,9 @@ topk_ragged_kernel(KArgs a) {
             if (sm.flag != 2u) return;
 
             // Finisher (its sm.cut0, cut1, tau0, tau1 are the row's endpoints).
+            // The counts and every candidate slot are loaded in one round
+            // trip (slots past the stored count hold stale words, ignored),
+            // all as agent-scope atomics.
             if (tid == 0) {
                 sm.cnt = __hip_atomic_load(&rs->count1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.cnt0 = __hip_atomic_load(&rs->count0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1501,6 +1651,15 @@ topk_ragged_kernel(KArgs a) {
                 sm.incomplete = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.amax = __hip_atomic_load(&rs->amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            uint32_t vi[kPer], vk[kPer];
+#pragma unroll
+            for (int j = 0; j < kPer; j++) {
+                const uint64_t v = __hip_atomic_load(&gc[j * kBlock + tid], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                vi[j] = (uint32_t)v;
+                vk[j] = (uint32_t)(v >> 32);
+            }
+            clear_hist(sm);
             __syncthreads();
             C1 = sm.cnt;
             C0 = sm.cnt0;
@@ -1508,46 +1667,31 @@ topk_ragged_kernel(KArgs a) {
             incomplete = sm.incomplete != 0 || stored > (uint32_t)kFront;
             nstored = incomplete ? 0u : stored;
             segmented = false;
-            // The merged frontier into LDS: every load is issued before the
-            // first is used (one round trip), read as agent-scope atomics.
-            {
-                uint32_t vi[kPer], vk[kPer];
+            PHASE_MARK(a, 4);
+            if (!incomplete &&
+                finish_split_fast(a, sm, r, nv, C0, C1, sm.amax, nstored, vi, vk)) {
+                PHASE_MARK(a, 5);
+                if (tid == 0) reset_row_state(rs);
+                return;
+            }
+            // general finish: the merged frontier into LDS
+            __syncthreads();
 #pragma unroll
-                for (int j = 0; j < kPer; j++) {
-                    const uint32_t t = (uint32_t)(j * kBlock + tid);
-                    uint64_t v = 0u;
-                    if (t < nstored)
-                        v = __hip_atomic_load(&gc[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    vi[j] = (uint32_t)v;
-                    vk[j] = (uint32_t)(v >> 32);
-                }
-#pragma unroll
-                for (int j = 0; j < kPer; j++) {
-                    const uint32_t t = (uint32_t)(j * kBlock + tid);
-                    if (t < nstored) {
-                        sm.ci[t] = vi[j];
-                        sm.ck[t] = vk[j];
-                    }
+            for (int j = 0; j < kPer; j++) {
+                const uint32_t t = (uint32_t)(j * kBlock + tid);
+                if (t < nstored) {
+                    sm.ci[t] = vi[j];
+                    sm.ck[t] = vk[j];
                 }
             }
             __syncthreads();
-            PHASE_MARK(a, 4);
         }
     }
 
     finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored);
     PHASE_MARK(a, 5);
 
-    if (split && tid == 0) {
-        // Leave the row state zeroed for the next call (graph replays).
-        __hip_atomic_store(&rs->count1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->count0, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->stored, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (split && tid == 0) reset_row_state(rs);
 }
 
 // Workspace set-up: header and zeroed per-row state (the candidate arrays
