@@ -1113,16 +1113,26 @@ __device__ __forceinline__ int64_t view_size(int64_t L, uint32_t a, int s_log2) 
     return ((int64_t)a < L) ? (L - a + s - 1) >> s_log2 : 0;
 }
 
+// floor(x / y) for y >= 1, exact: with x = n y + r (0 < r < y) the quotient
+// is 1/y below n + 1, and since (n + 1) y <= x + y < 2^33 that gap exceeds
+// half an FP64 ulp of n + 1, so the rounded quotient stays below n + 1.
+__device__ __forceinline__ uint32_t udiv32(uint32_t x, uint32_t y) {
+    return (uint32_t)floor((double)x / (double)y);
+}
+
 // Sum of max(L_r, 0) over all rows of the call (every workgroup of a
 // splittable call computes it to size its row's segments); len0 is this
 // thread's first term, lens[threadIdx.x] (0 past the last row), loaded
 // by the caller ahead of time.  Ends with a barrier.
 __device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm, int32_t len0) {
-    int64_t s = (int64_t)max(len0, 0);
-    for (int t = threadIdx.x + kBlock; t < a.n_rows; t += kBlock) s += (int64_t)max(a.lens[t], 0);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-    if (lane_id() == 0) sm.lsum[threadIdx.x >> 6] = s;
+    uint64_t s = (uint64_t)max(len0, 0);
+    for (int t = threadIdx.x + kBlock; t < a.n_rows; t += kBlock) s += (uint64_t)max(a.lens[t], 0);
+    // s < 2^53: wave sums of its bits [0,16), [16,32), [32,53) each fit 32 bits
+    const uint32_t lo = wave_incl_scan((uint32_t)s & 0xFFFFu);
+    const uint32_t mid = wave_incl_scan((uint32_t)(s >> 16) & 0xFFFFu);
+    const uint32_t hi = wave_incl_scan((uint32_t)(s >> 32));
+    if (lane_id() == 63)
+        sm.lsum[threadIdx.x >> 6] = (int64_t)lo + ((int64_t)mid << 16) + ((int64_t)hi << 32);
     __syncthreads();
     int64_t tot = 0;
 #pragma unroll
@@ -1529,10 +1539,18 @@ topk_ragged_kernel(KArgs a) {
             const int64_t total = block_total_length(a, sm, tid < a.n_rows ? len0_raw : 0);
             const int64_t items = a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
                                                              : (a.seg_items + 1) / 2;
-            const int64_t target = max((total + items - 1) / items, (int64_t)kSegMin);
-            const int64_t P0 = min((int64_t)a.pmax, (L + target - 1) / target);
-            seg = (((L + P0 - 1) / P0) + 63) & ~(int64_t)63;
-            P = (L + seg - 1) / seg;
+            // Divisions in FP64 (a few instructions, where 64-bit integer
+            // division takes hundreds).  target and P0 may be off by one
+            // after rounding: any target >= kSegMin and any P0 in
+            // [1, ceil(L / kSegMin)] make a valid plan, and every segment of
+            // the row computes the same one.  seg and P are exact (udiv32).
+            const double tq = ceil((double)total / (double)items);
+            const uint32_t target = (uint32_t)fmax((double)kSegMin, fmin(tq, 2147483648.0));
+            const uint32_t L32 = (uint32_t)L;
+            const uint32_t P0 = min((uint32_t)a.pmax, (uint32_t)ceil((double)L32 / (double)target));
+            const uint32_t seg32 = (udiv32(L32 + P0 - 1u, P0) + 63u) & ~63u;
+            seg = seg32;
+            P = udiv32(L32 + seg32 - 1u, seg32);
         }
         if (p >= P) return;
         split = P > 1;
