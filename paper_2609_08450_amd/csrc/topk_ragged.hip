@@ -101,7 +101,7 @@ struct KArgs {
     int32_t l_samp_min;
     int32_t cap;
 #ifdef TOPK_PHASE_TIMERS
-    uint64_t *timers; // 16 words per workgroup, see PHASE_MARK
+    uint64_t *timers; // 32 words per workgroup, see PHASE_MARK
 #endif
 };
 
@@ -1357,16 +1357,20 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     // histogram of the live keys (sm.hist and its group sums are clear);
     // tl[j]: key offset in the window, ~0 for a slot that is not live (the
     // window spans less than 2^32 - 1 keys, so ~0 is no live offset)
+    // (slot groups j with j * kBlock >= n hold no entry: skipped uniformly)
     uint32_t tl[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
-        const uint32_t t = ~asc_key(vk[j]) - win.klo;
-        const bool lv = (uint32_t)(j * kBlock + tid) < n && t <= win.kspan;
-        tl[j] = lv ? t : 0xFFFFFFFFu;
-        if (lv) {
-            const uint32_t d = t >> win.wf;
-            atomicAdd(&sm.hist[d], 1u);
-            atomicAdd(&sm.coarse[0][d >> 5], 1u);
+        tl[j] = 0xFFFFFFFFu;
+        if ((uint32_t)(j * kBlock) < n) {
+            const uint32_t t = ~asc_key(vk[j]) - win.klo;
+            const bool lv = (uint32_t)(j * kBlock + tid) < n && t <= win.kspan;
+            if (lv) {
+                tl[j] = t;
+                const uint32_t d = t >> win.wf;
+                atomicAdd(&sm.hist[d], 1u);
+                atomicAdd(&sm.coarse[0][d >> 5], 1u);
+            }
         }
     }
     if (tid == 0) sm.knext = 0u;
@@ -1392,7 +1396,8 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     const uint32_t kw = ce - cb; // keep iff tl - cb <= kw (never for ~0: ce < ~0)
     uint32_t cw = 0;
 #pragma unroll
-    for (int j = 0; j < kPer; j++) cw += (uint32_t)__popcll(__ballot(tl[j] < cend));
+    for (int j = 0; j < kPer; j++)
+        if ((uint32_t)(j * kBlock) < n) cw += (uint32_t)__popcll(__ballot(tl[j] < cend));
     if (lane == 0) sm.wc[w8] = cw;
     __syncthreads();
     PHASE_MARK(a, 11);
@@ -1405,6 +1410,7 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
+        if ((uint32_t)(j * kBlock) >= n) continue;
         const bool commit = tl[j] < cend;
         const uint64_t mc = __ballot(commit);
         if (commit) {
@@ -1429,6 +1435,7 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     }
     PHASE_MARK(a, 12);
     PHASE_WORD(a, 30, f.eq);
+    PHASE_WORD(a, 15, n);
     if (!take_all) {
         __syncthreads();
         rank_small(a, out0, zs, f.eq, need, f.below);
