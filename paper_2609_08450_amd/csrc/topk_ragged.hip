@@ -1605,6 +1605,26 @@ topk_ragged_kernel(KArgs a) {
         __syncthreads();
         C1 = sm.cnt;
         incomplete = sm.incomplete != 0;
+        // Split rows publish this segment's entries and counts
+        // (eq:method:split-local), then arrive; the last arrival merges them
+        // (eq:method:split-reduce) and finishes the row.  The segment's slots
+        // in the row's merged array are reserved first, so that the atomic's
+        // round trip overlaps the C(tau0) count.
+        // this wave's stored entries, those of the waves before it, all
+        const uint32_t w8 = (uint32_t)tid >> 6;
+        uint32_t wcnt = 0, wpre = 0, nst = 0, resv = 0;
+        if (split) {
+#pragma unroll
+            for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
+                const uint32_t c = min(sm.wcnt[v], (uint32_t)kWaveCap);
+                wcnt = v == w8 ? c : wcnt;
+                wpre += v < w8 ? c : 0u;
+                nst += c;
+            }
+            if (tid == 0 && nst)
+                resv = __hip_atomic_fetch_add(&rs->stored, nst, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+        }
         // C(tau0): from the stored A(tau1) entries, or by re-reading this
         // segment when a wave region overflowed.
         C0 = incomplete ? count_range(sm, a.scores, off, beg, end, sm.cut0)
@@ -1613,24 +1633,8 @@ topk_ragged_kernel(KArgs a) {
         PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)P << 16) | ((uint64_t)r << 32));
 
         if (split) {
-            // Publish this segment's entries and counts (eq:method:split-local),
-            // then arrive; the last arrival merges them (eq:method:split-reduce)
-            // and finishes the row.
-            // this wave's stored entries, those of the waves before it, all
-            const uint32_t w8 = (uint32_t)tid >> 6;
-            uint32_t wcnt = 0, wpre = 0, nst = 0;
-#pragma unroll
-            for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
-                const uint32_t c = min(sm.wcnt[v], (uint32_t)kWaveCap);
-                wcnt = v == w8 ? c : wcnt;
-                wpre += v < w8 ? c : 0u;
-                nst += c;
-            }
             if (tid == 0) {
-                sm.base = nst ? __hip_atomic_fetch_add(&rs->stored, nst,
-                                                               __ATOMIC_RELAXED,
-                                                               __HIP_MEMORY_SCOPE_AGENT)
-                                      : 0u;
+                sm.base = resv;
                 if (C1) __hip_atomic_fetch_add(&rs->count1, C1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (C0) __hip_atomic_fetch_add(&rs->count0, C0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (incomplete)
