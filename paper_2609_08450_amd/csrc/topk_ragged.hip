@@ -706,8 +706,11 @@ struct Classifier {
 // Writes output slot pos of this refinement (entry e, class known).
 __device__ __forceinline__ void put_out(const KArgs a, int64_t out0, uint32_t pos, uint32_t idx,
                                         uint32_t bits) {
-    a.out_idx[out0 + pos] = (int32_t)idx;
-    a.out_val[out0 + pos] = __builtin_bit_cast(float, bits);
+    // pos < K <= 16384: a 32-bit byte offset from the row's (uniform) base
+    const uint32_t boff = pos << 2;
+    *reinterpret_cast<int32_t *>(reinterpret_cast<char *>(a.out_idx + out0) + boff) = (int32_t)idx;
+    *reinterpret_cast<float *>(reinterpret_cast<char *>(a.out_val + out0) + boff) =
+        __builtin_bit_cast(float, bits);
 }
 
 // Ranks the nk keys of the LDS table zs against each other and writes the k
@@ -1405,8 +1408,6 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
 #pragma unroll
     for (uint32_t v = 0; v < (uint32_t)kWaves; v++) cbase += v < w8 ? sm.wc[v] : 0u;
     const int64_t out0 = (int64_t)r * a.K;
-    int32_t *oi = a.out_idx + out0;
-    float *ov = a.out_val + out0;
     uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
@@ -1416,8 +1417,7 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
         if (commit) {
             const uint32_t pos = cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
                                                __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u));
-            oi[pos] = (int32_t)vi[j];
-            ov[pos] = __builtin_bit_cast(float, vk[j]);
+            put_out(a, out0, pos, vi[j], vk[j]);
         }
         cbase += (uint32_t)__popcll(mc);
         const bool keep = !take_all && tl[j] - cb <= kw;
