@@ -292,6 +292,27 @@ __device__ __forceinline__ void wave_find_level2(const uint32_t *hist, uint32_t 
     if (lane == 0) { out->bin = (uint32_t)(owner * 32 + l2); out->below = below; out->eq = eq; }
 }
 
+// wave_find_level2 with the result returned (wave-uniform) instead of
+// stored, so that every wave can locate the bin itself.
+__device__ __forceinline__ Find wave_find_reg(const uint32_t *hist, uint32_t incl, uint32_t tot,
+                                              uint32_t total, uint32_t k) {
+    const int lane = lane_id();
+    Find f;
+    if (k == 0 || k > total) {
+        f.bin = kBins; f.below = total; f.eq = 0;
+        return f;
+    }
+    const int owner = __ffsll((unsigned long long)__ballot(incl >= k)) - 1;
+    const uint32_t base = __builtin_amdgcn_readlane(incl - tot, owner);
+    const uint32_t v = (lane < 32) ? hist[owner * 32 + lane] : 0u;
+    const uint32_t incl2 = wave_incl_scan(v);
+    const int l2 = __ffsll((unsigned long long)__ballot(lane < 32 && base + incl2 >= k)) - 1;
+    f.bin = (uint32_t)(owner * 32 + l2);
+    f.below = base + __builtin_amdgcn_readlane(incl2 - v, l2);
+    f.eq = __builtin_amdgcn_readlane(v, l2);
+    return f;
+}
+
 __device__ __forceinline__ void wave_find(const uint32_t *hist, uint32_t k0, uint32_t k1, int nk, Find *out) {
     const int lane = lane_id();
     const uint4 *h4 = reinterpret_cast<const uint4 *>(hist + lane * 32);
@@ -1379,15 +1400,15 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     if (tid == 0) sm.knext = 0u;
     __syncthreads();
     PHASE_MARK(a, 9);
-    if (tid < 64) {
-        const uint32_t c = sm.coarse[0][tid];
+    // every wave locates the boundary bin itself (no second barrier)
+    Find f;
+    {
+        const uint32_t c = sm.coarse[0][lane];
         const uint32_t incl = wave_incl_scan(c);
         const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
-        wave_find_level2(sm.hist, incl, c, total, K, &sm.find[0]);
+        f = wave_find_reg(sm.hist, incl, c, total, K);
     }
-    __syncthreads();
     PHASE_MARK(a, 10);
-    const Find f = sm.find[0];
     const uint32_t need = K - f.below;
     const bool take_all = f.eq == need;
     if (f.bin >= (uint32_t)kBins || (!take_all && f.eq > kSmall)) return false;
