@@ -1222,28 +1222,27 @@ __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, co
     for (; t < nv; t += kBlock) add(base[t << a.s_log2]);
     __syncthreads();
     PHASE_MARK(a, 18);
-    if (tid < 128) {
-        // wave 0 finds q0, wave 1 finds q1
+    // Every wave finds both boundaries itself and stores the same values
+    // into sm (each wave reads them back after its own store), so no
+    // barrier follows; thread 0 publishes them.  sm.hist stays dirty: every
+    // later user clears it first.
+    {
         const uint32_t c = sm.coarse[0][lane_id()];
         const uint32_t incl = wave_incl_scan(c);
         const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
-        const int which = tid >> 6;
-        wave_find_level2(sm.hist, incl, c, total, (uint32_t)(which ? a.q1 : a.q0), &sm.find[which]);
-    }
-    __syncthreads();
-    if (tid == 0) {
-        const uint32_t t0 = sm.find[0].bin, t1 = sm.find[1].bin;
-        if (pub)
+        const uint32_t t0 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q0).bin;
+        const uint32_t t1 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q1).bin;
+        if (tid == 0 && pub)
             __hip_atomic_store(pub, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-        sm.tau0 = t0;
-        sm.tau1 = t1;
-        sm.cut0 = bin_cutoff(t0);
-        sm.cut1 = bin_cutoff(t1);
+        if (lane_id() == 0) {
+            sm.tau0 = t0;
+            sm.tau1 = t1;
+            sm.cut0 = bin_cutoff(t0);
+            sm.cut1 = bin_cutoff(t1);
+        }
     }
-    __syncthreads();
     PHASE_MARK(a, 19);
-    clear_hist(sm);
 }
 
 // ---------------------------------------------------------- finish ----
