@@ -650,7 +650,9 @@ __device__ __forceinline__ void reset_range(Smem &sm) {
     if (threadIdx.x < 4) sm.red[threadIdx.x] = (threadIdx.x & 1) ? 0u : ~0u;
 }
 
-constexpr uint32_t kSmall = 512;
+// Ranking costs each of the ceil(n / 64) working waves n lane reads, so it
+// settles only small sets; a digit round is cheaper beyond about 64.
+constexpr uint32_t kSmall = 64;
 
 // The live key range of a round, [lo, hi] over composite keys, digit
 // d(z) = (z - lo) >> w.  When the range covers whole kappa32 values and the
