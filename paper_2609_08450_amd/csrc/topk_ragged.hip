@@ -38,8 +38,10 @@ constexpr int kBins = 2048;                 // 11-bit digits and coarse bins
 constexpr int kWaves = kBlock / 64;
 constexpr int kCap = TOPK_FRONTIER_CAP;     // largest policy frontier (pairs)
 constexpr int kFront = 7168;                // LDS frontier storage (pairs)
-constexpr int kWaveCap = kFront / kWaves - 1; // Phase 2 storage per wave (+1 spill slot)
+// Phase 2 region of a wave: kWaveCap entries, one spill slot, and 64 slots
+// (one per lane) that take the writes of lanes without a hit
 constexpr int kWaveStride = kFront / kWaves;
+constexpr int kWaveCap = kWaveStride - 1 - 64;
 static_assert(kCap <= kFront, "policy capacity must fit the storage");
 constexpr int kVec = 4;                     // 16-byte loads per thread per chunk
 static_assert(kVec * 4 <= 64, "per-thread element masks are 64-bit");
@@ -485,8 +487,7 @@ __device__ __forceinline__ void collect_range(Smem &sm, const float *scores, int
 // admitted tail.  Every value with ascending key u >= cut1 (the nested
 // boundary, so a C(tau0) < K proposal can take the band of
 // eq:method:rescue-band without a second traversal) is stored as (index, FP32
-// bits) in the private region of its wave: sm.ci/ck[w * kWaveCap ..), in
-// element order within the wave.  Each element costs one compare; a
+// bits) in the private region of its wave: sm.ci/ck[w * kWaveStride ..).  Each element costs one compare; a
 // wave-wide ballot places the hits with no atomics.  C(tau1) and C(tau0) are
 // counted exactly even where a wave region overflows (sm.incomplete is then
 // set).  The endpoints are read from sm after prologue() has run.
@@ -507,25 +508,33 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
                 // A positive endpoint v: x >= v iff the raw FP32 bits, read as
                 // signed integers, compare >= (one integer compare).
                 const int32_t t1 = (int32_t)bits_from_asc(cut1);
+                // Branch-free append: every lane writes every element, a hit
+                // to its slot (running count + rank among the vector
+                // element's hits), any other to its own dummy slot.
+                const uint32_t dummy = (uint32_t)kWaveCap + 1u + (uint32_t)lane_id();
 #pragma unroll
                 for (int m = 0; m < kVec; m++) if (m < mv) {
+                    bool hit[4];
+                    uint64_t mk[4];
 #pragma unroll
                     for (int c = 0; c < 4; c++) {
                         const uint32_t b = fbits(x[m][c]);
                         const bool h1 = kPos ? (int32_t)b >= t1 : asc_key(b) >= cut1;
-                        bool hit = h1;
-                        if constexpr (kEdge) hit = h1 && in_window(i0[m] + c, lo, hi);
-                        const uint64_t m1 = __ballot(hit);
-                        if (m1) {
-                            // slot kWaveCap of the region absorbs hits past its
-                            // capacity (the count stays exact)
-                            const uint32_t q = min(cur + __builtin_amdgcn_mbcnt_hi(
-                                                             (uint32_t)(m1 >> 32),
-                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m1, 0u)),
-                                                   (uint32_t)kWaveCap);
-                            if (hit) { wi[q] = (uint32_t)(i0[m] + c); wk[q] = b; }
-                            cur += (uint32_t)__popcll(m1);
-                        }
+                        hit[c] = h1;
+                        if constexpr (kEdge) hit[c] = h1 && in_window(i0[m] + c, lo, hi);
+                        mk[c] = __ballot(hit[c]);
+                    }
+#pragma unroll
+                    for (int c = 0; c < 4; c++) {
+                        // slot kWaveCap of the region absorbs hits past its
+                        // capacity (the count stays exact)
+                        const uint32_t q = min(__builtin_amdgcn_mbcnt_hi((uint32_t)(mk[c] >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mk[c], cur)),
+                                               (uint32_t)kWaveCap);
+                        const uint32_t d = hit[c] ? q : dummy;
+                        wi[d] = (uint32_t)(i0[m] + c);
+                        wk[d] = fbits(x[m][c]);
+                        cur += (uint32_t)__popcll(mk[c]);
                     }
                 }
             };
