@@ -1356,19 +1356,23 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     }
 }
 
-// Finish of a split row certified on the primary or band route, straight
-// from the merged candidates in registers (vi, vk: index and FP32 bits of
-// slot j * kBlock + tid, valid below n): one digit round over the live key
-// range [~amax, ~cut] (fine histogram plus 32-bin group sums, two-level
-// find), committed entries written out from registers in consecutive slots
-// of each wave, the boundary bin ranked when it holds at most kSmall
-// entries.  Returns false, having written nothing, when the row needs the
-// general finish (other routes, unknown range, a tiny or narrow frontier, a
-// large boundary bin).  Needs sm.hist and sm.coarse[0] clear.
-__device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r, int64_t nv,
-                                                  uint32_t C0, uint32_t C1, uint32_t amax,
-                                                  uint32_t n, const uint32_t (&vi)[kPer],
-                                                  const uint32_t (&vk)[kPer]) {
+// Finish of a row certified on the primary or band route, straight from its
+// candidates in registers (vi, vk: index and FP32 bits): one digit round over
+// the live key range [~amax, ~cut] (fine histogram plus 32-bin group sums,
+// two-level find), committed entries written out from registers in
+// consecutive slots of each wave, the boundary bin ranked when it holds at
+// most kSmall entries.  Slot (j, thread) holds a candidate iff j < ngroups
+// (block-uniform) and j * unit + pos < lim: the merged array of a split row
+// has unit = kBlock, pos = thread, lim = count; the per-wave regions of a
+// single workgroup have unit = 64, pos = lane, lim = the wave's count.
+// Returns false, having written nothing, when the row needs the general
+// finish (other routes, unknown range, a tiny or narrow frontier, a large
+// boundary bin).  Needs sm.hist and sm.coarse[0] clear.
+__device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int64_t nv,
+                                            uint32_t C0, uint32_t C1, uint32_t amax,
+                                            uint32_t unit, uint32_t pos, uint32_t lim,
+                                            uint32_t ngroups, const uint32_t (&vi)[kPer],
+                                            const uint32_t (&vk)[kPer]) {
     const int tid = threadIdx.x;
     const uint32_t lane = (uint32_t)lane_id(), w8 = (uint32_t)tid >> 6;
     const uint32_t K = (uint32_t)a.K, cap = (uint32_t)a.cap;
@@ -1391,14 +1395,14 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     // histogram of the live keys (sm.hist and its group sums are clear);
     // tl[j]: key offset in the window, ~0 for a slot that is not live (the
     // window spans less than 2^32 - 1 keys, so ~0 is no live offset)
-    // (slot groups j with j * kBlock >= n hold no entry: skipped uniformly)
+    // (slot groups j >= ngroups hold no entry: skipped uniformly)
     uint32_t tl[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
         tl[j] = 0xFFFFFFFFu;
-        if ((uint32_t)(j * kBlock) < n) {
+        if ((uint32_t)j < ngroups) {
             const uint32_t t = ~asc_key(vk[j]) - win.klo;
-            const bool lv = (uint32_t)(j * kBlock + tid) < n && t <= win.kspan;
+            const bool lv = (uint32_t)j * unit + pos < lim && t <= win.kspan;
             if (lv) {
                 tl[j] = t;
                 const uint32_t d = t >> win.wf;
@@ -1431,7 +1435,7 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     uint32_t cw = 0;
 #pragma unroll
     for (int j = 0; j < kPer; j++)
-        if ((uint32_t)(j * kBlock) < n) cw += (uint32_t)__popcll(__ballot(tl[j] < cend));
+        if ((uint32_t)j < ngroups) cw += (uint32_t)__popcll(__ballot(tl[j] < cend));
     if (lane == 0) sm.wc[w8] = cw;
     __syncthreads();
     PHASE_MARK(a, 11);
@@ -1442,7 +1446,7 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
-        if ((uint32_t)(j * kBlock) >= n) continue;
+        if ((uint32_t)j >= ngroups) continue;
         const bool commit = tl[j] < cend;
         const uint64_t mc = __ballot(commit);
         if (commit) {
@@ -1466,7 +1470,7 @@ __device__ __forceinline__ bool finish_split_fast(const KArgs a, Smem &sm, int r
     }
     PHASE_MARK(a, 12);
     PHASE_WORD(a, 30, f.eq);
-    PHASE_WORD(a, 15, n);
+    PHASE_WORD(a, 15, ngroups);
     if (!take_all) {
         __syncthreads();
         rank_small(a, out0, zs, f.eq, need, f.below);
@@ -1729,7 +1733,8 @@ topk_ragged_kernel(KArgs a) {
             segmented = false;
             PHASE_MARK(a, 4);
             if (!incomplete &&
-                finish_split_fast(a, sm, r, nv, C0, C1, sm.amax, nstored, vi, vk)) {
+                finish_fast(a, sm, r, nv, C0, C1, sm.amax, kBlock, (uint32_t)tid, nstored,
+                            (nstored + kBlock - 1) / kBlock, vi, vk)) {
                 PHASE_MARK(a, 5);
                 if (tid == 0) reset_row_state(rs);
                 return;
@@ -1748,6 +1753,34 @@ topk_ragged_kernel(KArgs a) {
         }
     }
 
+    if (sampled && !split && !incomplete) {
+        // A single workgroup's candidates, each wave's region into its own
+        // lanes' registers.
+        const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
+        const uint32_t cnt = min(sm.wcnt[w8], (uint32_t)kWaveCap);
+        uint32_t cmax = 0;
+#pragma unroll
+        for (uint32_t v = 0; v < (uint32_t)kWaves; v++) cmax = max(cmax, min(sm.wcnt[v], (uint32_t)kWaveCap));
+        uint32_t vi[kPer], vk[kPer];
+#pragma unroll
+        for (int j = 0; j < kPer; j++) {
+            const uint32_t e = (uint32_t)j * 64u + lane;
+            vi[j] = 0u;
+            vk[j] = 0u;
+            if (e < cnt) {
+                vi[j] = sm.ci[w8 * kWaveStride + e];
+                vk[j] = sm.ck[w8 * kWaveStride + e];
+            }
+        }
+        clear_hist(sm);
+        __syncthreads();
+        if (finish_fast(a, sm, r, nv, C0, C1, sm.amax, 64u, lane, cnt, (cmax + 63u) / 64u, vi,
+                        vk)) {
+            PHASE_MARK(a, 5);
+            return;
+        }
+        __syncthreads();
+    }
     finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored);
     PHASE_MARK(a, 5);
 
