@@ -102,8 +102,10 @@ int topk_ragged_default_policy(topk_ragged_policy *out);
 size_t topk_ragged_workspace_size(int32_t max_rows, int32_t K);
 
 /* One-time initialisation of a workspace of `bytes` bytes (enqueued on
- * `stream` with kernels only, no memset nodes).  Must run before the first
- * topk_ragged call on that workspace.  Kernels leave the workspace ready for
+ * `stream` with kernels only, no memset nodes).  The workspace must be
+ * 256-byte aligned, as hipMalloc returns (this call, topk_ragged and
+ * topk_ragged_read_stats return TOPK_EINVAL otherwise).  Must run before the
+ * first topk_ragged call on that workspace.  Kernels leave the workspace ready for
  * the next call, so graph replays need no re-initialisation. */
 int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, int32_t K,
                                void *stream);
@@ -119,8 +121,9 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
  *   K            1 <= K <= TOPK_K_MAX.
  *   out_idx      device, int32 [n_rows x K], row-relative indices.
  *   out_val      device, FP32 [n_rows x K], bit-exact copies of the scores.
- *   workspace    device, initialised by topk_ragged_workspace_init with
- *                max_rows >= n_rows; not shared by concurrent calls.
+ *   workspace    device, 256-byte aligned (as hipMalloc returns), initialised
+ *                by topk_ragged_workspace_init with max_rows >= n_rows; not
+ *                shared by concurrent calls.
  * Row lengths and offsets stay on the device; the launch geometry depends
  * only on (n_rows, K, device).  If the workspace is invalid for n_rows the
  * kernel writes -1 / -inf to every output and counts an error in the stats.

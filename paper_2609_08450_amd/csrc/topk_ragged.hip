@@ -54,6 +54,7 @@ constexpr uint32_t kMagic = 0x544F504Bu;    // workspace header tag
 constexpr int kSpinLimit = 1 << 15;         // polls before recomputing the view
 constexpr size_t kHeaderBytes = 1024;
 constexpr size_t kRowStateBytes = 256;
+constexpr uintptr_t kWorkspaceAlign = 256; // 64-bit atomics and 16-byte header loads
 constexpr size_t kRowBlockBytes = kRowStateBytes + 2 * kFront * sizeof(uint32_t);
 
 typedef float f4 __attribute__((ext_vector_type(4)));
@@ -64,11 +65,12 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 // (the segments' A(tau1) entries, concatenated).  Every field and entry is
 // written and read with agent-scope atomic accesses (see the arrive step).
 struct RowState {
+    uint64_t sa;         // entries reserved in the candidate buffer (low 32
+                         // bits) | segments done with Phase 2 << 32: the last
+                         // arrival's atomic returns the final reserved count
     uint32_t taus;       // segment 0's tau0 | tau1 << 16 | 1 << 31 once known
-    uint32_t arrive;     // segments done with Phase 2
     uint32_t count1;     // C(tau1) of the row (exact)
     uint32_t count0;     // C(tau0) of the row (exact)
-    uint32_t stored;     // entries reserved in the candidate buffer
     uint32_t incomplete; // a segment could not keep all of its A(tau1)
     uint32_t amax;       // largest ascending key among the stored entries
 };
@@ -1495,10 +1497,9 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
 __device__ __forceinline__ void reset_row_state(RowState *rs) {
     __hip_atomic_store(&rs->count1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->count0, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&rs->stored, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->sa, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&rs->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -1657,8 +1658,8 @@ topk_ragged_kernel(KArgs a) {
                 nst += c;
             }
             if (tid == 0 && nst)
-                resv = __hip_atomic_fetch_add(&rs->stored, nst, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
+                resv = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)nst, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
         }
         // C(tau0): from the stored A(tau1) entries, or by re-reading this
         // segment when a wave region overflowed.
@@ -1696,30 +1697,34 @@ topk_ragged_kernel(KArgs a) {
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid == 0) {
-                const uint32_t old = __hip_atomic_fetch_add(&rs->arrive, 1u, __ATOMIC_RELAXED,
+                const uint64_t old = __hip_atomic_fetch_add(&rs->sa, 1ull << 32, __ATOMIC_RELAXED,
                                                             __HIP_MEMORY_SCOPE_AGENT);
-                sm.flag = (old == (uint32_t)(P - 1)) ? 2u : 0u;
+                sm.flag = ((uint32_t)(old >> 32) == (uint32_t)(P - 1)) ? 2u : 0u;
+                sm.base = (uint32_t)old; // every segment has reserved by now
             }
             __syncthreads();
             PHASE_MARK(a, 3);
             if (sm.flag != 2u) return;
 
             // Finisher (its sm.cut0, cut1, tau0, tau1 are the row's endpoints).
-            // The counts and every candidate slot are loaded in one round
-            // trip (slots past the stored count hold stale words, ignored),
-            // all as agent-scope atomics.
+            // The counts and the slot groups that hold candidates are loaded
+            // in one round trip (slots past the stored count in the last
+            // group hold stale words, ignored), all as agent-scope atomics.
+            const uint32_t stored = sm.base;
+            const uint32_t ngroups = (min(stored, (uint32_t)kFront) + kBlock - 1) / kBlock;
             if (tid == 0) {
                 sm.cnt = __hip_atomic_load(&rs->count1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.cnt0 = __hip_atomic_load(&rs->count0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                sm.base = __hip_atomic_load(&rs->stored, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.incomplete = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.amax = __hip_atomic_load(&rs->amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             uint32_t vi[kPer], vk[kPer];
 #pragma unroll
             for (int j = 0; j < kPer; j++) {
-                const uint64_t v = __hip_atomic_load(&gc[j * kBlock + tid], __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
+                uint64_t v = 0;
+                if ((uint32_t)j < ngroups)
+                    v = __hip_atomic_load(&gc[j * kBlock + tid], __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
                 vi[j] = (uint32_t)v;
                 vk[j] = (uint32_t)(v >> 32);
             }
@@ -1727,14 +1732,13 @@ topk_ragged_kernel(KArgs a) {
             __syncthreads();
             C1 = sm.cnt;
             C0 = sm.cnt0;
-            const uint32_t stored = sm.base;
             incomplete = sm.incomplete != 0 || stored > (uint32_t)kFront;
             nstored = incomplete ? 0u : stored;
             segmented = false;
             PHASE_MARK(a, 4);
             if (!incomplete &&
                 finish_fast(a, sm, r, nv, C0, C1, sm.amax, kBlock, (uint32_t)tid, nstored,
-                            (nstored + kBlock - 1) / kBlock, vi, vk)) {
+                            ngroups, vi, vk)) {
                 PHASE_MARK(a, 5);
                 if (tid == 0) reset_row_state(rs);
                 return;
@@ -1909,6 +1913,7 @@ size_t topk_ragged_workspace_size(int32_t max_rows, int32_t K) {
 int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, int32_t K,
                                void *stream) {
     if (!workspace || max_rows < 0 || K < 1 || K > TOPK_K_MAX) return TOPK_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % kWorkspaceAlign) return TOPK_EINVAL;
     DeviceInfo di;
     const int st = device_info(&di);
     if (st != TOPK_OK) return st;
@@ -1939,6 +1944,7 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     if (n_rows == 0) return TOPK_OK;
     if (!scores || !row_offsets || !row_lengths || !out_idx || !out_val || !workspace)
         return TOPK_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % kWorkspaceAlign) return TOPK_EINVAL;
     const topk_ragged_policy pol = policy ? *policy : default_policy();
     if (pol.s_log2 < 0 || pol.s_log2 > 12 || pol.rho_num < 1 || pol.rho_den < 1 ||
         pol.rho1_num < 1 || pol.rho1_den < 1 || pol.cap < 1 || pol.cap > kCap)
@@ -1986,6 +1992,7 @@ int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *
 
 int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream) {
     if (!workspace || !out) return TOPK_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % kWorkspaceAlign) return TOPK_EINVAL;
     WsHeader *hdr = static_cast<WsHeader *>(workspace);
     uint32_t st[16];
     hipStream_t s = (hipStream_t)stream;

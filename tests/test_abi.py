@@ -53,6 +53,11 @@ def test_host_argument_checks(lib):
     assert lib.topk_ragged_workspace_size(-1, 2048) == 0
     assert lib.topk_ragged_workspace_size(4, 0) == 0
     assert lib.topk_ragged_workspace_init(n, 0, 4, 2048, n) == -1
+    # a workspace that is not 256-byte aligned is refused before any device work
+    assert lib.topk_ragged_workspace_init(P(4096 + 8), 1 << 20, 4, 2048, n) == -1
+    assert lib.topk_ragged(P(16), P(16), P(16), 4, 2048, P(16), P(16), P(4096 + 8), n) == -1
+    from paper_2609_08450_amd.topk import Stats
+    assert lib.topk_ragged_read_stats(P(4096 + 8), ctypes.byref(Stats()), n) == -1
     assert lib.topk_ragged_read_stats(n, n, n) == -1
     assert lib.topk_ragged_debug_cutoffs(n, n) == -1
     assert lib.topk_ragged_debug_coarse(n, -1, n, n) == -1
