@@ -751,8 +751,9 @@ __device__ __forceinline__ void put_out(const KArgs a, int64_t out0, uint32_t po
 // lowest to output slots placed + rank.  Wave v ranks table entries
 // [64 v, 64 v + 64) against the whole table, 64 keys at a time read across
 // lanes.  Needs the table complete (caller's barrier).
-__device__ __forceinline__ void rank_small(const KArgs a, int64_t out0, const uint64_t *zs,
-                                           uint32_t nk, uint32_t k, uint32_t placed) {
+template <class Sink>
+__device__ __forceinline__ void rank_small_to(const uint64_t *zs, uint32_t nk, uint32_t k,
+                                              uint32_t placed, Sink &&sink) {
     const uint32_t w8 = threadIdx.x >> 6, lane = (uint32_t)lane_id();
     if (64 * w8 >= nk) return;
     const uint32_t i = 64 * w8 + lane;
@@ -769,8 +770,14 @@ __device__ __forceinline__ void rank_small(const KArgs a, int64_t out0, const ui
             rank += (v < z) ? 1u : 0u;
         }
     }
-    if (i < nk && rank < k)
-        put_out(a, out0, placed + rank, (uint32_t)z, bits_from_asc(~(uint32_t)(z >> 32)));
+    if (i < nk && rank < k) sink(placed + rank, (uint32_t)z, bits_from_asc(~(uint32_t)(z >> 32)));
+}
+
+__device__ __forceinline__ void rank_small(const KArgs a, int64_t out0, const uint64_t *zs,
+                                           uint32_t nk, uint32_t k, uint32_t placed) {
+    rank_small_to(zs, nk, k, placed, [&](uint32_t pos, uint32_t idx, uint32_t bits) {
+        put_out(a, out0, pos, idx, bits);
+    });
 }
 
 // Per-wave exclusive prefix and total of sm.wc / sm.wk (after a barrier).
@@ -1358,6 +1365,29 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     }
 }
 
+// Writes the K (index, FP32 bits) pairs staged in sm.ci/ck[0, K) to row
+// output out0: 16-byte stores when both output rows are 16-byte aligned,
+// else 4-byte ones (consecutive lanes, consecutive slots either way).
+__device__ __forceinline__ void store_staged(const KArgs a, const Smem &sm, int64_t out0) {
+    const uint32_t K = (uint32_t)a.K;
+    int32_t *oi = a.out_idx + out0;
+    float *ov = a.out_val + out0;
+    if (((reinterpret_cast<uintptr_t>(oi) | reinterpret_cast<uintptr_t>(ov)) & 15u) == 0 &&
+        (K & 3u) == 0) {
+        const uint4 *si = reinterpret_cast<const uint4 *>(sm.ci);
+        const uint4 *sk = reinterpret_cast<const uint4 *>(sm.ck);
+        for (uint32_t e = threadIdx.x; e < K / 4; e += kBlock) {
+            reinterpret_cast<uint4 *>(oi)[e] = si[e];
+            reinterpret_cast<uint4 *>(ov)[e] = sk[e];
+        }
+    } else {
+        for (uint32_t e = threadIdx.x; e < K; e += kBlock) {
+            oi[e] = (int32_t)sm.ci[e];
+            ov[e] = __builtin_bit_cast(float, sm.ck[e]);
+        }
+    }
+}
+
 // Finish of a row certified on the primary or band route, straight from its
 // candidates in registers (vi, vk: index and FP32 bits): one digit round over
 // the live key range [~amax, ~cut] (fine histogram plus 32-bin group sums,
@@ -1446,6 +1476,8 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
     for (uint32_t v = 0; v < (uint32_t)kWaves; v++) cbase += v < w8 ? sm.wc[v] : 0u;
     const int64_t out0 = (int64_t)r * a.K;
     uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
+    // committed entries are staged in sm.ci/ck[0, K) (free in this path: the
+    // candidates are in registers; K <= n_live <= cap < kFront)
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
         if ((uint32_t)j >= ngroups) continue;
@@ -1454,7 +1486,8 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
         if (commit) {
             const uint32_t pos = cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
                                                __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u));
-            put_out(a, out0, pos, vi[j], vk[j]);
+            sm.ci[pos] = vi[j];
+            sm.ck[pos] = vk[j];
         }
         cbase += (uint32_t)__popcll(mc);
         const bool keep = !take_all && tl[j] - cb <= kw;
@@ -1475,8 +1508,15 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
     PHASE_WORD(a, 15, ngroups);
     if (!take_all) {
         __syncthreads();
-        rank_small(a, out0, zs, f.eq, need, f.below);
+        rank_small_to(zs, f.eq, need, f.below, [&](uint32_t pos, uint32_t idx, uint32_t bits) {
+            sm.ci[pos] = idx;
+            sm.ck[pos] = bits;
+        });
     }
+    // The K outputs were staged in LDS (slot order is free): write them out
+    // with few, wide stores.
+    __syncthreads();
+    store_staged(a, sm, out0);
     PHASE_MARK(a, 13);
     if (tid == 0) {
         atomicAdd(&a.hdr->stats[route], 1u);
