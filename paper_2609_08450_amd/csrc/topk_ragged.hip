@@ -55,13 +55,20 @@ constexpr int kSpinLimit = 1 << 15;         // polls before recomputing the view
 constexpr size_t kHeaderBytes = 1024;
 constexpr size_t kRowStateBytes = 256;
 constexpr uintptr_t kWorkspaceAlign = 256; // 64-bit atomics and 16-byte header loads
-constexpr size_t kRowBlockBytes = kRowStateBytes + 2 * kFront * sizeof(uint32_t);
+constexpr size_t kViewHistBytes = kBins * sizeof(uint32_t); // a split row's merged view histogram
+constexpr size_t kRowBlockBytes = kRowStateBytes + kViewHistBytes + 2 * kFront * sizeof(uint32_t);
+// Views of at least this many samples are shared by a split row's segments
+// (each histograms the samples inside its own range and the histograms are
+// merged): one workgroup gathering them all is bound by its cache-line
+// fills (one 128-byte line per 4-byte sample).
+constexpr int64_t kCoopView = 4096;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 // Per-row state of a split row.  Row r of a split call owns the workspace
 // block at kHeaderBytes + r * kRowBlockBytes: this state, padded to 256
-// bytes, then kFront candidates as 64-bit (index | FP32 bits << 32) words
+// bytes, the 2048-bin view histogram that segments sharing the view add
+// into, then kFront candidates as 64-bit (index | FP32 bits << 32) words
 // (the segments' A(tau1) entries, concatenated).  Every field and entry is
 // written and read with agent-scope atomic accesses (see the arrive step).
 struct RowState {
@@ -73,6 +80,7 @@ struct RowState {
     uint32_t count0;     // C(tau0) of the row (exact)
     uint32_t incomplete; // a segment could not keep all of its A(tau1)
     uint32_t amax;       // largest ascending key among the stored entries
+    uint32_t varrive;    // segments that have added their part of a shared view
 };
 
 // Workspace header (first kHeaderBytes of the workspace).
@@ -330,6 +338,21 @@ __device__ __forceinline__ void wave_find(const uint32_t *hist, uint32_t k0, uin
     const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
     wave_find_level2(hist, incl, tot, total, k0, &out[0]);
     if (nk > 1) wave_find_level2(hist, incl, tot, total, k1, &out[1]);
+}
+
+// Sums of the 64 groups of 32 bins of a 2048-bin histogram into out[64], by
+// the whole block: thread t adds bins [4 t, 4 t + 4), then each group of 8
+// lanes is summed with DPP row shifts (lane 8 g + 7 holds group g's sum).
+// Needs the histogram complete (caller's barrier); out is complete after the
+// next barrier.
+static_assert(kBlock * 4 == kBins, "group_sums: one uint4 of bins per thread");
+__device__ __forceinline__ void group_sums(const uint32_t *hist, uint32_t *out) {
+    const uint4 h = reinterpret_cast<const uint4 *>(hist)[threadIdx.x];
+    uint32_t v = h.x + h.y + h.z + h.w;
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xf, 0xf, false); // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xf, 0xf, false); // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xf, 0xf, false); // row_shr:4
+    if ((threadIdx.x & 7u) == 7u) out[threadIdx.x >> 3] = v;
 }
 
 // ------------------------------------------------- shared state ----
@@ -1265,6 +1288,99 @@ __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, co
     PHASE_MARK(a, 19);
 }
 
+// Shared view of a split row (Section 4.5 with the view partitioned over the
+// segments instead of re-read by each): segment p takes the view positions
+// a_r + k s inside its own range [beg, end), k in [k0, k1).
+__device__ __forceinline__ void coop_view_range(const KArgs a, int r, int32_t beg, int32_t end,
+                                                int64_t &k0, int64_t &k1) {
+    const int64_t ph = view_phase(r, a.s_log2), s = (int64_t)1 << a.s_log2;
+    k0 = beg > ph ? (beg - ph + s - 1) >> a.s_log2 : 0;
+    k1 = end > ph ? (end - ph + s - 1) >> a.s_log2 : 0;
+}
+
+__device__ __forceinline__ void coop_view_issue(const KArgs a, int r, const float *row, int64_t k0,
+                                                int64_t k1, float (&xs)[kP1]) {
+    const float *base = row + view_phase(r, a.s_log2);
+#pragma unroll
+    for (int j = 0; j < kP1; j++) {
+        const int64_t k = k0 + threadIdx.x + (int64_t)j * kBlock;
+        xs[j] = 0.0f;
+        if (k < k1) xs[j] = base[k << a.s_log2];
+    }
+}
+
+// Histograms this segment's view samples (sm.hist clear before a preceding
+// barrier), adds the non-zero bins into the row's view histogram vh, and
+// arrives; the last segment to arrive loads the merged histogram, clears vh,
+// finds tau0 and tau1 (eq:method:sample-hist, eq:method:primary-threshold)
+// and publishes them in rs->taus, and returns true with them in sm.  The
+// others return false (they poll rs->taus).  The merged histogram is that of
+// the whole view, so the boundaries are the ones segment 0 alone would find.
+__device__ __forceinline__ bool coop_view_finish(const KArgs a, Smem &sm, int r, const float *row,
+                                                 int64_t k0, int64_t k1, const float (&xs)[kP1],
+                                                 RowState *rs, uint32_t *vh, int64_t P) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < kP1; j++) {
+        const int64_t k = k0 + tid + (int64_t)j * kBlock;
+        if (k < k1) atomicAdd(&sm.hist[coarse_bin(xs[j])], 1u);
+    }
+    const float *base = row + view_phase(r, a.s_log2);
+    for (int64_t k = k0 + tid + (int64_t)kP1 * kBlock; k < k1; k += kBlock)
+        atomicAdd(&sm.hist[coarse_bin(base[k << a.s_log2])], 1u);
+    __syncthreads();
+    {
+        const uint4 h = reinterpret_cast<const uint4 *>(sm.hist)[tid];
+        uint32_t *d = vh + 4 * tid;
+        if (h.x) __hip_atomic_fetch_add(d + 0, h.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (h.y) __hip_atomic_fetch_add(d + 1, h.y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (h.z) __hip_atomic_fetch_add(d + 2, h.z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (h.w) __hip_atomic_fetch_add(d + 3, h.w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // (as for the candidates: every wave's additions complete before the
+    // barrier that precedes the arrival)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(&rs->varrive, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        sm.flag = old == (uint32_t)(P - 1) ? 2u : 0u;
+    }
+    __syncthreads();
+    if (sm.flag != 2u) return false;
+    {
+        uint64_t *d = reinterpret_cast<uint64_t *>(vh + 4 * tid);
+        const uint64_t lo = __hip_atomic_load(d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t hi = __hip_atomic_load(d + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        reinterpret_cast<uint4 *>(sm.hist)[tid] =
+            make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32));
+        // cleared for the next call once read (the values are in LDS now)
+        __hip_atomic_store(d, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(d + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (tid == 0) __hip_atomic_store(&rs->varrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    group_sums(sm.hist, sm.coarse[0]);
+    __syncthreads();
+    {
+        const uint32_t c = sm.coarse[0][lane_id()];
+        const uint32_t incl = wave_incl_scan(c);
+        const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+        const uint32_t t0 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q0).bin;
+        const uint32_t t1 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q1).bin;
+        if (tid == 0)
+            __hip_atomic_store(&rs->taus, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        if (lane_id() == 0) {
+            sm.tau0 = t0;
+            sm.tau1 = t1;
+            sm.cut0 = bin_cutoff(t0);
+            sm.cut1 = bin_cutoff(t1);
+        }
+    }
+    return true;
+}
+
 // ---------------------------------------------------------- finish ----
 
 // Certification and the routes after Phase 2 (Section 4.3).  For a sampled
@@ -1541,6 +1657,7 @@ __device__ __forceinline__ void reset_row_state(RowState *rs) {
     __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->varrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void
@@ -1598,8 +1715,10 @@ topk_ragged_kernel(KArgs a) {
 
     RowState *rs = reinterpret_cast<RowState *>(a.rows + (size_t)r * kRowBlockBytes);
     // the row's merged candidates: index | FP32 bits << 32
-    uint64_t *gc = reinterpret_cast<uint64_t *>(a.rows + (size_t)r * kRowBlockBytes +
+    uint32_t *vh = reinterpret_cast<uint32_t *>(a.rows + (size_t)r * kRowBlockBytes +
                                                 kRowStateBytes);
+    uint64_t *gc = reinterpret_cast<uint64_t *>(a.rows + (size_t)r * kRowBlockBytes +
+                                                kRowStateBytes + kViewHistBytes);
     uint32_t C0 = 0, C1 = 0, nstored = 0;
     bool incomplete = false, segmented = true, split = false;
 
@@ -1610,9 +1729,11 @@ topk_ragged_kernel(KArgs a) {
         if (tid == 0) { sm.cnt = 0; sm.cnt0 = 0; sm.incomplete = 0; sm.amax = 0; }
         // Segment 0 reads the view; its loads go out first, the segment plan
         // and the first chunk follow, and the view is histogrammed with that
-        // chunk in flight.
+        // chunk in flight.  A large view of a split row is shared instead:
+        // each segment reads the part inside its own range (after the plan).
         float xs[kP1];
-        if (p == 0) phase1_issue(a, r, row, L, xs);
+        const bool big_view = nv >= kCoopView && a.pmax > 1;
+        if (p == 0 && !big_view) phase1_issue(a, r, row, L, xs);
         // Segments: when rows may be split, a row is cut into P0 =
         // min(pmax, ceil(L / target)) pieces of equal length rounded up to 64
         // elements, target = max(kSegMin, sum(L) / items), so that the call
@@ -1639,6 +1760,14 @@ topk_ragged_kernel(KArgs a) {
         split = P > 1;
         const int32_t beg = (int32_t)(p * seg);
         const int32_t end = (int32_t)min(L, p * seg + seg);
+        const bool coop = split && big_view;
+        int64_t k0 = 0, k1 = 0;
+        if (coop) {
+            coop_view_range(a, r, beg, end, k0, k1);
+            coop_view_issue(a, r, row, k0, k1, xs);
+        } else if (p == 0 && big_view) {
+            phase1_issue(a, r, row, L, xs); // not split: the whole view, after the plan
+        }
         // Phase 2 over this segment: certify against cut0 and keep A(tau1).
         // The endpoints come from segment 0, which publishes tau0 and tau1 in
         // one agent-scope atomic word (the endpoints follow from the bins);
@@ -1648,8 +1777,14 @@ topk_ragged_kernel(KArgs a) {
         // segment 0 is dispatched before any other segment, so the wait ends.
         PHASE_MARK(a, 16);
         phase2_collect(sm, a.scores, off, beg, end, [&]() {
-            bool own = p == 0;
-            if (!own) {
+            bool have = false; // endpoints in sm
+            if (coop) {
+                have = coop_view_finish(a, sm, r, row, k0, k1, xs, rs, vh, P);
+            } else if (p == 0) {
+                phase1_finish(a, sm, r, row, L, xs, split ? &rs->taus : nullptr);
+                have = true;
+            }
+            if (!have) {
                 if (tid == 0) {
                     uint32_t v = 0;
                     for (int spin = 0; spin < kSpinLimit; spin++) {
@@ -1671,11 +1806,14 @@ topk_ragged_kernel(KArgs a) {
                 }
                 __syncthreads();
                 if (sm.flag == 0u) {
-                    own = true;
+                    // the whole view, on its own (sm.hist may hold this
+                    // segment's part of a shared view)
+                    clear_hist(sm);
+                    __syncthreads();
                     phase1_issue(a, r, row, L, xs);
+                    phase1_finish(a, sm, r, row, L, xs, nullptr);
                 }
             }
-            if (own) phase1_finish(a, sm, r, row, L, xs, split && p == 0 ? &rs->taus : nullptr);
             PHASE_MARK(a, 1);
         });
         __syncthreads();
@@ -1837,7 +1975,8 @@ __global__ void ws_init_kernel(WsHeader *hdr, char *rows, uint32_t split_rows, u
                                uint32_t cap) {
     for (uint32_t r = blockIdx.x; r < split_rows; r += gridDim.x) {
         uint32_t *w = reinterpret_cast<uint32_t *>(rows + (size_t)r * kRowBlockBytes);
-        if (threadIdx.x < kRowStateBytes / 4) w[threadIdx.x] = 0;
+        for (uint32_t i = threadIdx.x; i < (kRowStateBytes + kViewHistBytes) / 4; i += blockDim.x)
+            w[i] = 0;
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         hdr->split_rows = split_rows;

@@ -355,3 +355,44 @@ def test_graph_capture_and_replay(topk):
                                   where=f"replay {rep} call {j}")
     ri, rv = oracle.topk_ragged(wa.scores, wa.row_offsets, wa.row_lengths, K)
     assert_same_selection(*eager[0], ri, rv, where="eager vs oracle")
+
+
+def test_outputs_not_16_byte_aligned(topk):
+    """Output rows that start off the 16-byte grid (4-byte aligned views)
+    take the 4-byte store path of the staged write-out."""
+    import torch
+
+    wl = W.decode(n_rows=12)
+    say("decode 12 rows, outputs offset by one element")
+    s, o, l = device_arrays(wl)
+    n, K = wl.n_rows, wl.K
+    ws = topk.alloc_workspace(n, K)
+    bi = torch.full((n * K + 1,), -7, dtype=torch.int32, device="cuda")
+    bv = torch.full((n * K + 1,), 7.0, dtype=torch.float32, device="cuda")
+    oi_d, ov_d = bi[1:], bv[1:]
+    assert oi_d.data_ptr() % 16 != 0
+    topk.topk_ragged(s, o, l, n, K, oi_d, ov_d, ws)
+    torch.cuda.synchronize()
+    assert int(bi[0]) == -7 and float(bv[0]) == 7.0   # nothing written before the rows
+    gi = oi_d.view(n, K).cpu().numpy()
+    gv = ov_d.view(n, K).cpu().numpy()
+    oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, K)
+    assert_same_selection(gi, gv, oi, ov, where="unaligned outputs")
+
+
+def test_shared_view_rows(topk):
+    """Split rows whose view is large enough to be shared by their segments
+    (each histograms the view positions in its own range, the last merges):
+    the boundaries, routes and selections must equal the oracle's."""
+    rng = np.random.default_rng(23)
+    lens = np.array([524288, 700001, 1048576, 600000, 530000], np.int32)
+    rows = []
+    for i, L in enumerate(lens):
+        x = W.decode_mixture_row(rng, int(L))
+        if i == 3:
+            x = np.round(x * 8.0).astype(np.float32) / 8.0      # heavy ties
+        rows.append(x.astype(np.float32))
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    for K in (2048, 300):
+        wl = W.Workload(f"shared view K={K}", np.concatenate(rows), offs, lens, K, "")
+        parity(topk, wl)
