@@ -152,6 +152,147 @@ def traffic_summary(paths, config: int, copy_mib: int, out_path: str):
     print(json.dumps(out))
 
 
+def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0):
+    """Times `steps` topk_ragged calls on workload wl (policy None = default)
+    over rotated device copies, captured in graphs and replayed on one stream
+    between HIP events.  Returns (ms per call, route counts of one call,
+    copies, calls per graph, warm-up calls)."""
+    import torch
+
+    from paper_2609_08450_amd import topk
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    K, n = wl.K, wl.n_rows
+    batch_bytes = 4 * wl.scores.size
+    copies = max(1, -(-ROTATE_MIN_BYTES // batch_bytes)) if rotate else 1
+    stream = torch.cuda.Stream(device=dev)
+
+    with torch.cuda.stream(stream):
+        host = torch.from_numpy(wl.scores)
+        bufs = [host.to(dev) for _ in range(copies)]
+        offs = torch.from_numpy(wl.row_offsets).to(dev)
+        lens = torch.from_numpy(wl.row_lengths).to(dev)
+        out_idx = torch.empty((n, K), dtype=torch.int32, device=dev)
+        out_val = torch.empty((n, K), dtype=torch.float32, device=dev)
+        ws = topk.alloc_workspace(n, K, dev, stream)
+    stream.synchronize()
+
+    def call(i, s):
+        if policy is None:
+            topk.topk_ragged(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws, s)
+        else:
+            topk.topk_ragged_ex(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws,
+                                policy, None, s)
+
+    # one graph with G consecutive calls over rotating copies; a tail graph for
+    # the remainder, so exactly `steps` calls are timed
+    G = calls_per_graph or copies
+    G = max(1, min(G, steps)) if steps > 0 else 1
+
+    def capture(ncalls, first):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for j in range(ncalls):
+                call(first + j, torch.cuda.current_stream())
+        return g
+
+    with torch.cuda.stream(stream):
+        for i in range(min(warmup, 3)):
+            call(i, stream)           # eager warm-up (code object load)
+    stream.synchronize()
+    g_main = capture(G, 0)
+    rem = steps % G
+    g_tail = capture(rem, 0) if rem else None
+    stream.synchronize()
+
+    def run(nsteps):
+        reps, tail = divmod(nsteps, G)
+        for _ in range(reps):
+            g_main.replay()
+        if tail:
+            assert tail == rem
+            g_tail.replay()
+
+    # warmup: whole graph replays plus the tail, untimed
+    wreps = max(1, warmup // G)
+    for _ in range(wreps):
+        g_main.replay()
+    torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        run(steps)
+        ev1.record(stream)
+    ev1.synchronize()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+
+    # outside the timed region: route counts of one call
+    topk.read_stats(ws, stream)
+    with torch.cuda.stream(stream):
+        call(0, stream)
+    routes = topk.read_stats(ws, stream)
+    del bufs, g_main, g_tail
+    torch.cuda.synchronize()
+    return ms / steps, routes, copies, G, wreps * G
+
+
+ABLATIONS = ("margin", "stride", "rescue", "crossover", "k")
+
+
+def ablation(name, wl, steps, warmup):
+    """The paper's policy ablations (Section 6: retention margin, sampling
+    stride, conditional rescue, sampled-versus-exact crossover) and other K,
+    on synthetic rows: per variant the time per call and the route counts."""
+    from paper_2609_08450_amd import topk
+    from paper_2609_08450_amd import workloads as W
+
+    base = topk.default_policy()
+
+    def pol(**kw):
+        p = topk.Policy(**base.as_dict())
+        for k, v in kw.items():
+            setattr(p, k, v)
+        return p
+
+    def with_k(w, K):
+        return W.Workload(f"{w.name} K={K}", w.scores, w.row_offsets, w.row_lengths, K,
+                          w.description)
+
+    variants = []
+    if name == "margin":      # K~ = rho K at s = 128, primary only (rho1 = rho)
+        for num, den in ((1, 1), (5, 4), (3, 2), (7, 4), (2, 1)):
+            variants.append((f"rho={num}/{den}", wl,
+                             pol(rho_num=num, rho_den=den, rho1_num=num, rho1_den=den)))
+    elif name == "stride":    # s from 16 to 256 at rho = 3/2, primary only
+        for sl in (4, 5, 6, 7, 8):
+            variants.append((f"s={1 << sl}", wl, pol(s_log2=sl, rho1_num=3, rho1_den=2)))
+    elif name == "rescue":    # nested band (rho1 = 7/4) against primary only
+        variants = [("rescue rho1=7/4", wl, base), ("primary only", wl, pol(rho1_num=3, rho1_den=2))]
+    elif name == "crossover": # fixed-length decode rows, sampled against exact route
+        for L in (8192, 16384, 32768, 65536, 131072):
+            rng = np.random.default_rng(260908450 + L)
+            rows = [W.decode_mixture_row(rng, L).astype(np.float32) for _ in range(64)]
+            lens = np.full(64, L, np.int32)
+            offs = (np.arange(64, dtype=np.int64) * L)
+            wlL = W.Workload(f"64 rows L={L}", np.concatenate(rows), offs, lens, 2048, "decode mixture")
+            variants.append((f"L={L} sampled", wlL, pol(l_samp_min=0)))
+            variants.append((f"L={L} exact", wlL, pol(l_samp_min=0x7FFFFFFF)))
+    elif name == "k":
+        for K in (256, 512, 1024, 2048, 4096):
+            variants.append((f"K={K}", with_k(wl, K), base))
+    for label, w, p in variants:
+        ms, routes, copies, _, _ = time_calls(w, p, steps, warmup)
+        print(json.dumps({"ablation": name, "variant": label, "rows": w.n_rows, "K": w.K,
+                          "us_per_call": round(ms * 1e3, 3),
+                          "gbs": round(4.0 * w.total_len / (ms * 1e-3) / 1e9, 2),
+                          "routes": routes, "policy": p.as_dict()}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,6 +309,9 @@ def main():
                     help="kernel FETCH_SIZE, kernel WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE "
                          "counter CSVs from rocprofv3 --pmc; writes the traffic file and exits")
     ap.add_argument("--copy-mib", type=int, default=1024, help="size of the calibration copy")
+    ap.add_argument("--ablation", choices=ABLATIONS, default=None,
+                    help="instead of the bench line, one JSON line per policy variant (the "
+                         "paper's ablations on synthetic rows; --config picks the rows)")
     args = ap.parse_args()
 
     if args.traffic_summary:
@@ -184,85 +328,16 @@ def main():
         copy_calibration(args.copy_calibration, max(1, args.steps), args.warmup)
         return
 
-    import torch
-
-    from paper_2609_08450_amd import topk
-
-    dev = torch.device("cuda", 0)
-    torch.cuda.set_device(dev)
     wl = make_workload(args.config)
+    if args.ablation:
+        ablation(args.ablation, wl, args.steps, args.warmup)
+        return
+    ms_per_step, routes, copies, G, wreps = time_calls(wl, None, args.steps, args.warmup,
+                                                       not args.no_rotate, args.calls_per_graph)
     K, n = wl.K, wl.n_rows
     batch_bytes = 4 * wl.scores.size
-    copies = 1 if args.no_rotate else max(1, -(-ROTATE_MIN_BYTES // batch_bytes))
-    stream = torch.cuda.Stream(device=dev)
-
-    with torch.cuda.stream(stream):
-        host = torch.from_numpy(wl.scores)
-        bufs = [host.to(dev) for _ in range(copies)]
-        offs = torch.from_numpy(wl.row_offsets).to(dev)
-        lens = torch.from_numpy(wl.row_lengths).to(dev)
-        out_idx = torch.empty((n, K), dtype=torch.int32, device=dev)
-        out_val = torch.empty((n, K), dtype=torch.float32, device=dev)
-        ws = topk.alloc_workspace(n, K, dev, stream)
-    stream.synchronize()
-
-    def call(i, s):
-        topk.topk_ragged(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws, s)
-
-    # one graph with G consecutive calls over rotating copies; a tail graph for
-    # the remainder, so exactly `steps` calls are timed
-    G = args.calls_per_graph or copies
-    G = max(1, min(G, args.steps)) if args.steps > 0 else 1
-
-    def capture(ncalls, first):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=stream):
-            for j in range(ncalls):
-                call(first + j, torch.cuda.current_stream())
-        return g
-
-    with torch.cuda.stream(stream):
-        for i in range(min(args.warmup, 3)):
-            call(i, stream)           # eager warm-up (code object load)
-    stream.synchronize()
-    g_main = capture(G, 0)
-    rem = args.steps % G
-    g_tail = capture(rem, 0) if rem else None
-    stream.synchronize()
-
-    def run(nsteps):
-        reps, tail = divmod(nsteps, G)
-        for _ in range(reps):
-            g_main.replay()
-        if tail:
-            assert tail == rem
-            g_tail.replay()
-
-    # warmup: whole graph replays plus the tail, untimed
-    wreps = max(1, args.warmup // G)
-    for _ in range(wreps):
-        g_main.replay()
-    torch.cuda.synchronize()
-
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        ev0.record(stream)
-        run(args.steps)
-        ev1.record(stream)
-    ev1.synchronize()
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1)
-    ms_per_step = ms / args.steps
     alg_bytes = 4.0 * wl.total_len
     gbs = alg_bytes / (ms_per_step * 1e-3) / 1e9
-
-    # outside the timed region: route counts of one call and a parity spot check
-    topk.read_stats(ws, stream)
-    with torch.cuda.stream(stream):
-        call(0, stream)
-    routes = topk.read_stats(ws, stream)
 
     traffic = measured_traffic(args.config)
     result = {
@@ -271,7 +346,7 @@ def main():
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": wreps * G,
+        "warmup": wreps,
         "ms_per_step": round(ms_per_step, 6),
         "us_per_call": round(ms_per_step * 1e3, 3),
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
