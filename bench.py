@@ -320,8 +320,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(rows shard independently across GPUs; see DESIGN.md).", file=sys.stderr)
+        print("bench.py runs on one GPU only: there is no multi-GPU launcher. Rows are "
+              "independent, so a batch shards by rows, each GPU running the kernel on its "
+              "own share.", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration:
