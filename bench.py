@@ -241,7 +241,7 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0):
     return ms / steps, routes, copies, G, wreps * G
 
 
-ABLATIONS = ("margin", "stride", "rescue", "crossover", "k")
+ABLATIONS = ("margin", "stride", "rescue", "crossover", "k", "recal", "recal-crossover")
 
 
 def ablation(name, wl, steps, warmup):
@@ -282,9 +282,36 @@ def ablation(name, wl, steps, warmup):
             wlL = W.Workload(f"64 rows L={L}", np.concatenate(rows), offs, lens, 2048, "decode mixture")
             variants.append((f"L={L} sampled", wlL, pol(l_samp_min=0)))
             variants.append((f"L={L} exact", wlL, pol(l_samp_min=0x7FFFFFFF)))
-    elif name == "k":
+    elif name == "k":         # the K = 2048 constants against the per-K policy
+        for K in (256, 512, 1024, 2048, 4096, 8192):
+            variants.append((f"K={K} evaluated constants", with_k(wl, K), base))
+            variants.append((f"K={K} per-K policy", with_k(wl, K), topk.policy_for_k(K)))
+    elif name == "recal":     # other K: stride and margins around the sample rank
+        for K, pairs in ((256, ((3, 2, 7, 4), (2, 1, 5, 2), (3, 1, 4, 1))),
+                         (512, ((3, 2, 7, 4), (2, 1, 5, 2), (3, 1, 4, 1))),
+                         (1024, ((3, 2, 7, 4), (2, 1, 5, 2), (3, 1, 4, 1))),
+                         (4096, ((5, 4, 11, 8), (4, 3, 3, 2), (3, 2, 7, 4)))):
+            for sl in (4, 5, 6, 7):
+                for rn, rd, r1n, r1d in pairs:
+                    variants.append((f"K={K} s={1 << sl} rho={rn}/{rd} rho1={r1n}/{r1d}",
+                                     with_k(wl, K),
+                                     pol(s_log2=sl, rho_num=rn, rho_den=rd, rho1_num=r1n,
+                                         rho1_den=r1d)))
+    elif name == "recal-crossover":  # per-K policy: sampled against exact on short rows
         for K in (256, 512, 1024, 2048, 4096):
-            variants.append((f"K={K}", with_k(wl, K), base))
+            kp = topk.policy_for_k(K).as_dict()
+            for m in (2, 4, 8, 16, 32):
+                L = m * K
+                if L > 131072:
+                    continue
+                rng = np.random.default_rng(260908450 + L + K)
+                rows = [W.decode_mixture_row(rng, L).astype(np.float32) for _ in range(64)]
+                lens = np.full(64, L, np.int32)
+                offs = (np.arange(64, dtype=np.int64) * L)
+                wlL = W.Workload(f"64 rows L={L}", np.concatenate(rows), offs, lens, K,
+                                 "decode mixture")
+                variants.append((f"K={K} L={L} sampled", wlL, pol(**dict(kp, l_samp_min=0))))
+                variants.append((f"K={K} L={L} exact", wlL, pol(l_samp_min=0x7FFFFFFF)))
     for label, w, p in variants:
         ms, routes, copies, _, _ = time_calls(w, p, steps, warmup)
         print(json.dumps({"ablation": name, "variant": label, "rows": w.n_rows, "K": w.K,

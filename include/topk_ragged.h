@@ -51,8 +51,10 @@ extern "C" {
 #define TOPK_EWORKSPACE (-4)   /* workspace too small for the plan */
 
 /* Largest supported K.  Results are exact for every K up to this value; the
- * sampled pipeline is tuned for K around 2048 (K~ = 1.5 K candidates must fit
- * the on-chip frontier of TOPK_FRONTIER_CAP entries). */
+ * sampled pipeline needs its candidates (about K~ = 1.5 K at K = 2048) to fit
+ * the on-chip frontier of TOPK_FRONTIER_CAP entries, so the per-K policy
+ * (topk_ragged_policy_for_k) sends every row of a larger K to the exact
+ * route. */
 #define TOPK_K_MAX 16384
 /* Frontier capacity of one workgroup, in (index, key) pairs. */
 #define TOPK_FRONTIER_CAP 6144
@@ -92,8 +94,23 @@ typedef struct topk_ragged_stats {
     uint64_t errors;       /* calls rejected on the device (bad workspace) */
 } topk_ragged_stats;
 
-/* Fills *out with the default policy.  Returns TOPK_OK. */
+/* Fills *out with the evaluated configuration above (the policy for K
+ * around 2048).  Returns TOPK_OK. */
 int topk_ragged_default_policy(topk_ragged_policy *out);
+
+/* Fills *out with the policy used for this K when none is given.  Section 4.5
+ * leaves the coarse target, its sample rank and the candidate budget to be
+ * recalibrated per K; measured on synthetic decode rows:
+ *   K < 384:           sample ranks 8 and 10 (K~ = 1024, K~1 = 1280);
+ *   384 <= K < 768:    K~ = 3 K,   K~1 = 4 K;
+ *   768 <= K < 2048:   K~ = 2 K,   K~1 = 5/2 K;
+ *   2048 <= K < 2560:  the evaluated configuration;
+ *   2560 <= K < 4352:  s = 16, K~ = 5/4 K, K~1 = 11/8 K;
+ *   4352 <= K:         every row takes the exact route (l_samp_min = INT32_MAX);
+ * s = 128 unless stated; the sampling floor is 4 K from K = 2048 and 8192
+ * elements below (shorter rows measured faster on the exact route).  Returns TOPK_OK, or
+ * TOPK_EINVAL for a null pointer or K outside [1, TOPK_K_MAX]. */
+int topk_ragged_policy_for_k(int32_t K, topk_ragged_policy *out);
 
 /* Bytes of workspace needed for calls with n_rows <= max_rows and this K on
  * the current device.  Independent of row lengths: per-row state is kept only
@@ -132,7 +149,8 @@ int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *
                 int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                 void *stream);
 
-/* topk_ragged with an explicit policy (NULL = default) and an optional
+/* topk_ragged with an explicit policy (NULL = topk_ragged_policy_for_k(K),
+ * which is also what topk_ragged uses) and an optional
  * per-row trace (device, int32 [n_rows x TOPK_TRACE_WORDS], NULL = none):
  *   [0] route (TOPK_ROUTE_*, TOPK_ROUTE_REREAD_FLAG or-ed in), [1] view size
  *   |V| (-1 if L <= K), [2] tau0, [3] tau1 (-1 if not sampled), [4] C(tau0),

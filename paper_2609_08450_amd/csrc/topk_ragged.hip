@@ -2067,6 +2067,43 @@ topk_ragged_policy default_policy() {
     return p;
 }
 
+// The constants recalibrated for other K (Section 4.5: the coarse target, its
+// sample rank and the candidate budget depend on K, the correctness argument
+// does not), measured on synthetic decode rows.  Below K = 2048 the view
+// stays at s = 128 and the margins widen as K shrinks, so that the sample
+// ranks keep an underfilled proposal no likelier than in the evaluated
+// configuration (sample ranks 8 and 10 at least); from K = 2560 the budget is
+// tight, so s = 16 sharpens the estimate under margins of 5/4 and 11/8; from
+// K = 4352 even those would overflow the frontier too often (C(tau0) above the
+// capacity on about 1 row in 100), so every row takes the exact route.  Below
+// K = 2048 rows shorter than 8192 take the exact route as well: there the
+// candidates are a large share of a short row, span a wide key range, and
+// the exact route measured faster.
+topk_ragged_policy policy_for_k(int32_t K) {
+    topk_ragged_policy p = default_policy();
+    if (K < 2048) p.l_samp_min = 8192;
+    if (K >= 4352) {
+        p.l_samp_min = 0x7FFFFFFF;
+    } else if (K >= 2560) {
+        p.s_log2 = 4;
+        p.rho_num = 5; p.rho_den = 4;
+        p.rho1_num = 11; p.rho1_den = 8;
+    } else if (K >= 2048) {
+        // the evaluated configuration
+    } else if (K >= 768) {
+        p.rho_num = 2; p.rho_den = 1;
+        p.rho1_num = 5; p.rho1_den = 2;
+    } else if (K >= 384) {
+        p.rho_num = 3; p.rho_den = 1;
+        p.rho1_num = 4; p.rho1_den = 1;
+    } else {
+        // sample ranks 8 and 10 at s = 128
+        p.rho_num = 8 << 7; p.rho_den = K;
+        p.rho1_num = 10 << 7; p.rho1_den = K;
+    }
+    return p;
+}
+
 int32_t sample_rank(int32_t K, int32_t num, int32_t den, int32_t s_log2) {
     const int64_t d = (int64_t)den << s_log2;
     return (int32_t)(((int64_t)num * K + d - 1) / d);
@@ -2079,6 +2116,12 @@ extern "C" {
 int topk_ragged_default_policy(topk_ragged_policy *out) {
     if (!out) return TOPK_EINVAL;
     *out = default_policy();
+    return TOPK_OK;
+}
+
+int topk_ragged_policy_for_k(int32_t K, topk_ragged_policy *out) {
+    if (!out || K < 1 || K > TOPK_K_MAX) return TOPK_EINVAL;
+    *out = policy_for_k(K);
     return TOPK_OK;
 }
 
@@ -2124,7 +2167,7 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     if (!scores || !row_offsets || !row_lengths || !out_idx || !out_val || !workspace)
         return TOPK_EINVAL;
     if (reinterpret_cast<uintptr_t>(workspace) % kWorkspaceAlign) return TOPK_EINVAL;
-    const topk_ragged_policy pol = policy ? *policy : default_policy();
+    const topk_ragged_policy pol = policy ? *policy : policy_for_k(K);
     if (pol.s_log2 < 0 || pol.s_log2 > 12 || pol.rho_num < 1 || pol.rho_den < 1 ||
         pol.rho1_num < 1 || pol.rho1_den < 1 || pol.cap < 1 || pol.cap > kCap)
         return TOPK_EINVAL;

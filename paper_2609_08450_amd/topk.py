@@ -94,6 +94,8 @@ def lib():
         L.topk_ragged_read_stats.restype = ctypes.c_int
         L.topk_ragged_default_policy.argtypes = [ctypes.POINTER(Policy)]
         L.topk_ragged_default_policy.restype = ctypes.c_int
+        L.topk_ragged_policy_for_k.argtypes = [ctypes.c_int32, ctypes.POINTER(Policy)]
+        L.topk_ragged_policy_for_k.restype = ctypes.c_int
         L.topk_ragged_debug_coarse.argtypes = [P, i64, P, P]
         L.topk_ragged_debug_coarse.restype = ctypes.c_int
         L.topk_ragged_debug_cutoffs.argtypes = [P, P]
@@ -129,8 +131,16 @@ def _stream(stream):
 
 
 def default_policy() -> Policy:
+    """The evaluated configuration (the policy for K around 2048)."""
     p = Policy()
     _check(lib().topk_ragged_default_policy(ctypes.byref(p)), "topk_ragged_default_policy")
+    return p
+
+
+def policy_for_k(K: int) -> Policy:
+    """The policy a call with this K uses when none is given."""
+    p = Policy()
+    _check(lib().topk_ragged_policy_for_k(K, ctypes.byref(p)), "topk_ragged_policy_for_k")
     return p
 
 

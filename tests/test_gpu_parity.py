@@ -31,13 +31,14 @@ def say(*a):
     print("[case]", *a, flush=True)
 
 
-def parity(topk, wl, policy=None, trace=True, where=""):
+def parity(topk, wl, policy=None, trace=True, where="", per_k=False):
+    """per_k: call without a policy (the library's topk_ragged_policy_for_k)."""
     import torch
 
     say(where or wl.name, "rows", wl.n_rows, "sum L", wl.total_len, "K", wl.K)
     s, o, l = device_arrays(wl)
-    pol = policy or topk.default_policy()
-    gi, gv, gt, st = run_hip(s, o, l, wl.K, pol, trace)
+    pol = topk.policy_for_k(wl.K) if per_k else (policy or topk.default_policy())
+    gi, gv, gt, st = run_hip(s, o, l, wl.K, None if per_k else pol, trace)
     oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, wl.K)
     assert_same_selection(gi, gv, oi, ov, where=where or wl.name)
     if trace:
@@ -396,3 +397,22 @@ def test_shared_view_rows(topk):
     for K in (2048, 300):
         wl = W.Workload(f"shared view K={K}", np.concatenate(rows), offs, lens, K, "")
         parity(topk, wl)
+
+
+@pytest.mark.parametrize("K", [1, 7, 100, 256, 383, 384, 512, 1000, 1024, 1600, 2047, 2500,
+                               2560, 3000, 4096, 4351, 4352, 6000])
+def test_parity_per_k_policy(topk, K):
+    """Calls without a policy use the per-K constants (topk_ragged_policy_for_k):
+    decode-mixture rows around the sampling floor and up to 131072 elements,
+    selections and per-row routes against the oracle under that policy."""
+    rng = np.random.default_rng(1000 + K)
+    lens = sorted({max(1, K - 1), K + 1, 4 * K - 1, 4 * K, 4 * K + 7, 10 * K + 3, 16384, 40000,
+                   90001, 131072})
+    rows = [W.decode_mixture_row(rng, int(L)).astype(np.float32) for L in lens]
+    lens = np.array(lens, np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload(f"per-K policy K={K}", np.concatenate(rows), offs, lens, K, "")
+    gt, st = parity(topk, wl, per_k=True)
+    say("routes", st)
+    if K >= 4352:
+        assert st["primary"] + st["band"] == 0
