@@ -123,16 +123,25 @@ struct KArgs {
 // has the merged frontier, 5 row done; word 6 = hardware id, 7 = role;
 // 8 finish entered, 9 frontier ready, 10..12 after refinement rounds 0..2,
 // 13 refinement done, 14 live entries entering refinement, 15 rounds run.
+// The stamps go to LDS and are copied out when the workgroup exits, so that
+// no global store of the instrumentation delays the loads being timed.
 #ifdef TOPK_PHASE_TIMERS
+__shared__ uint64_t g_tmarks[32];
 #define PHASE_MARK(a, k)                                                                 \
     do {                                                                                 \
-        if ((a).timers && threadIdx.x == 0)                                              \
-            (a).timers[(size_t)blockIdx.x * 32 + (k)] = wall_clock64();                   \
+        if ((a).timers && threadIdx.x == 0) g_tmarks[k] = wall_clock64();                \
     } while (0)
 #define PHASE_WORD(a, k, v)                                                              \
     do {                                                                                 \
-        if ((a).timers && threadIdx.x == 0) (a).timers[(size_t)blockIdx.x * 32 + (k)] = (v); \
+        if ((a).timers && threadIdx.x == 0) g_tmarks[k] = (v);                           \
     } while (0)
+struct TimerFlush {
+    uint64_t *t;
+    __device__ ~TimerFlush() {
+        if (t && threadIdx.x == 0)
+            for (int k = 0; k < 32; k++) t[(size_t)blockIdx.x * 32 + k] = g_tmarks[k];
+    }
+};
 #else
 #define PHASE_MARK(a, k) do {} while (0)
 #define PHASE_WORD(a, k, v) do {} while (0)
@@ -410,13 +419,60 @@ struct NoPrologue {
     __device__ void operator()() const {}
 };
 
+// A row range as 16-byte vectors: [beg, end) of the row at element offset
+// off, covered by nvec vectors from vbase (aligned down to 16 bytes; ibase is
+// the row index of vbase's first element), in nch chunks of kChunkVecs.
+struct RowVecs {
+    const char *vbase;
+    int32_t ibase, nvec, nch;
+};
+
+__device__ __forceinline__ RowVecs row_vecs(const float *scores, int64_t off, int32_t beg,
+                                            int32_t end) {
+    const uintptr_t sp = reinterpret_cast<uintptr_t>(scores);
+    const int64_t sh = (int64_t)((sp & 15) >> 2);
+    const int64_t v0 = (off + beg + sh) >> 2;
+    RowVecs g;
+    g.nvec = (int32_t)(((off + end + sh + 3) >> 2) - v0);
+    g.vbase = reinterpret_cast<const char *>(sp & ~(uintptr_t)15) + v0 * 16;
+    g.ibase = (int32_t)(v0 * 4 - sh - off);
+    g.nch = (g.nvec + kChunkVecs - 1) / kChunkVecs;
+    return g;
+}
+
+// Loads of chunk c are unconditional: lanes and chunks past the end re-read
+// the last vector of the range (one cache line per wave), masked later by
+// the window test, so that the in-order load counter lets each consume wait
+// for its own chunk only.
+template <bool kNT>
+__device__ __forceinline__ void issue_chunk(const RowVecs &g, f4 *dst, int32_t c) {
+    const int32_t cb = c * kChunkVecs;
+#pragma unroll
+    for (int m = 0; m < kVec; m++) {
+        const int32_t vi = min(cb + m * kBlock + (int32_t)threadIdx.x, g.nvec - 1);
+        dst[m] = load4<kNT>(reinterpret_cast<const f4 *>(g.vbase + (uint32_t)vi * 16u));
+    }
+}
+
+template <class F>
+__device__ __forceinline__ void consume_chunk(const RowVecs &g, const f4 *src, int32_t c,
+                                              int32_t beg, int32_t end, F &fn) {
+    if (c >= g.nch) return;
+    const int32_t cb = c * kChunkVecs;
+    // vectors of this chunk per thread (block-uniform)
+    const int32_t mv = min(kVec, (g.nvec - cb + kBlock - 1) / kBlock);
+    int32_t i0[kVec];
+#pragma unroll
+    for (int m = 0; m < kVec; m++) i0[m] = g.ibase + (cb + m * kBlock + (int32_t)threadIdx.x) * 4;
+    // interior chunks need no per-element window test
+    const bool edge = g.ibase + cb * 4 < beg || g.ibase + (cb + mv * kBlock) * 4 > end;
+    fn(src, i0, beg, end, edge, mv);
+}
+
 // Double-buffered chunks: while one chunk (kVec 16-byte loads per thread) is
-// consumed, the next one is in flight.  Loads are unconditional -- lanes and
-// chunks past the end re-read the last vector of the range (one cache line per
-// wave), masked by the window test -- so the in-order load counter lets each
-// consume wait for its own chunk only.  prologue() runs once, by every thread,
-// with the first chunk in flight (loads it waits for must have been issued
-// before the call, or they would queue behind the chunk).
+// consumed, the next one is in flight.  prologue() runs once, by every
+// thread, with the first chunk in flight (loads it waits for must have been
+// issued before the call, or they would queue behind the chunk).
 template <bool kNT, class F, class Pro = NoPrologue>
 __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int32_t beg,
                                            int32_t end, F &&fn, Pro &&prologue = Pro()) {
@@ -424,43 +480,37 @@ __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int
         prologue();
         return;
     }
-    const uintptr_t sp = reinterpret_cast<uintptr_t>(scores);
-    const int64_t sh = (int64_t)((sp & 15) >> 2);
-    const int64_t v0 = (off + beg + sh) >> 2;
-    const int32_t nvec = (int32_t)(((off + end + sh + 3) >> 2) - v0);
-    const char *vbase = reinterpret_cast<const char *>(sp & ~(uintptr_t)15) + v0 * 16;
-    const int32_t ibase = (int32_t)(v0 * 4 - sh - off); // row index of vbase's first element
-    const int32_t nch = (nvec + kChunkVecs - 1) / kChunkVecs;
-    const int tid = threadIdx.x;
+    const RowVecs g = row_vecs(scores, off, beg, end);
     f4 xa[kVec], xb[kVec];
-    auto issue = [&](f4 *dst, int32_t c) {
-        const int32_t cb = c * kChunkVecs;
-#pragma unroll
-        for (int m = 0; m < kVec; m++) {
-            const int32_t vi = min(cb + m * kBlock + tid, nvec - 1);
-            dst[m] = load4<kNT>(reinterpret_cast<const f4 *>(vbase + (uint32_t)vi * 16u));
-        }
-    };
-    auto consume = [&](const f4 *src, int32_t c) {
-        if (c >= nch) return;
-        const int32_t cb = c * kChunkVecs;
-        // vectors of this chunk per thread (block-uniform)
-        const int32_t mv = min(kVec, (nvec - cb + kBlock - 1) / kBlock);
-        int32_t i0[kVec];
-#pragma unroll
-        for (int m = 0; m < kVec; m++) i0[m] = ibase + (cb + m * kBlock + tid) * 4;
-        // interior chunks need no per-element window test
-        const bool edge = ibase + cb * 4 < beg || ibase + (cb + mv * kBlock) * 4 > end;
-        fn(src, i0, beg, end, edge, mv);
-    };
-    issue(xa, 0);
+    issue_chunk<kNT>(g, xa, 0);
     prologue();
-    for (int32_t c = 0; c < nch; c += 2) {
-        issue(xb, c + 1);
-        consume(xa, c);
-        issue(xa, c + 2);
-        consume(xb, c + 1);
+    for (int32_t c = 0; c < g.nch; c += 2) {
+        issue_chunk<kNT>(g, xb, c + 1);
+        consume_chunk(g, xa, c, beg, end, fn);
+        issue_chunk<kNT>(g, xa, c + 2);
+        consume_chunk(g, xb, c + 1, beg, end, fn);
     }
+}
+
+// Largest range resident_row takes, in chunks.
+constexpr int kResidentChunks = 2;
+
+// A range of at most kResidentChunks chunks held in registers: both chunks
+// are loaded once and passed to fn1, then mid() runs (every thread, may
+// synchronise), then the same registers are passed to fn2 -- a two-pass
+// computation that reads the range from memory once.
+template <class F1, class M, class F2>
+__device__ __forceinline__ void resident_row(const RowVecs &g, int32_t beg, int32_t end, F1 &&fn1,
+                                             M &&mid, F2 &&fn2) {
+    static_assert(kResidentChunks == 2, "two register chunks");
+    f4 xa[kVec], xb[kVec];
+    issue_chunk<false>(g, xa, 0);
+    issue_chunk<false>(g, xb, 1);
+    consume_chunk(g, xa, 0, beg, end, fn1);
+    consume_chunk(g, xb, 1, beg, end, fn1);
+    mid();
+    consume_chunk(g, xa, 0, beg, end, fn2);
+    consume_chunk(g, xb, 1, beg, end, fn2);
 }
 
 __device__ __forceinline__ bool in_window(int32_t i, int32_t lo, int32_t hi) {
@@ -1120,48 +1170,128 @@ __device__ __forceinline__ void reread_select(const KArgs a, Smem &sm, int r, in
 // Exact coarse recovery (eq:method:exact-init) over the whole row by this
 // workgroup: a coarse histogram pass finds tau_star = min{b : C(b) >= K}; a
 // classify pass commits c < tau_star to the output (E0) and keeps
-// c == tau_star as the frontier Q0 when it fits the capacity.  Returns
-// (tau_star, |E0|, |Q0|) in sm.find[0]; ends with a barrier, sm.hist cleared.
+// c == tau_star as the frontier Q0 when it fits the capacity.  A row of at
+// most kResidentChunks chunks is read once and both passes run from
+// registers; a longer one is streamed twice.  Returns (tau_star, |E0|, |Q0|)
+// in sm.find[0]; ends with a barrier, sm.hist cleared.
 __device__ __forceinline__ void exact_classify(const KArgs a, Smem &sm, int r, int64_t off, int64_t L) {
     const int tid = threadIdx.x;
-    const float *scores = a.scores;
-    stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                      int32_t hi, bool, int32_t mv) {
+    auto hist = [&](const f4 *x, const int32_t *i0, int32_t lo, int32_t hi, bool edge,
+                    int32_t mv) {
 #pragma unroll
         for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++)
-                if (in_window(i0[m] + c, lo, hi)) atomicAdd(&sm.hist[coarse_bin(x[m][c])], 1u);
+                if (!edge || in_window(i0[m] + c, lo, hi))
+                    atomicAdd(&sm.hist[coarse_bin(x[m][c])], 1u);
         }
-    });
-    __syncthreads();
-    if (tid < 64) wave_find(sm.hist, (uint32_t)a.K, 0, 1, sm.find);
-    if (tid == 0) sm.cnt = 0;
-    __syncthreads();
-    const uint32_t tstar = sm.find[0].bin;
-    const bool fits = sm.find[0].eq <= (uint32_t)a.cap;
-    stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                      int32_t hi, bool, int32_t mv) {
+    };
+    // After the find: c < tau_star iff u >= key_hi, c == tau_star iff
+    // key_lo <= u < key_hi (the bins' ascending-key endpoints); an empty
+    // keep range when the bin does not fit the frontier.  When E0 and Q0 fit
+    // the LDS pairs together, E0 is staged at their top (e0_top on) and
+    // written out after the pass, so that the pass itself stores nothing to
+    // global memory (a store in the loop would make each wait for the next
+    // chunk's loads wait for the stores as well).
+    uint32_t key_lo = 0, key_hi = 0, e0_top = kFront, below = 0;
+    bool stage = false;
+    auto find = [&]() {
+        PHASE_MARK(a, 22);
+        __syncthreads();
+        PHASE_MARK(a, 23);
+        if (tid < 64) wave_find(sm.hist, (uint32_t)a.K, 0, 1, sm.find);
+        if (tid == 0) sm.cnt = 0;
+        __syncthreads();
+        PHASE_MARK(a, 24);
+        const uint32_t tstar = sm.find[0].bin;
+        const bool fits = sm.find[0].eq <= (uint32_t)a.cap;
+        key_hi = tstar > 0 ? bin_cutoff(tstar - 1) : 0xFFFFFFFFu;
+        key_lo = fits ? bin_cutoff(tstar) : key_hi;
+        below = sm.find[0].below;
+        stage = below + (fits ? sm.find[0].eq : 0u) <= (uint32_t)kFront;
+        e0_top = (uint32_t)kFront - below;
+    };
+    // Appends are wave-aggregated per chunk: each lane builds bit masks of
+    // its committed and kept elements, a wave scan of the two counts (packed
+    // in one word: at most 16 per lane) gives each lane its first slots, and
+    // lane 0 reserves the wave's total with one LDS atomic per category.
+    static_assert(kVec * 4 <= 16 && kWaves * 64 * 16 < 65536, "packed counts");
+    const int lane = lane_id();
+    int32_t *oi = a.out_idx + (int64_t)r * a.K;
+    float *ov = a.out_val + (int64_t)r * a.K;
+    auto classify = [&](const f4 *x, const int32_t *i0, int32_t lo, int32_t hi, bool edge,
+                        int32_t mv) {
+        uint32_t mlt = 0, meq = 0;
 #pragma unroll
         for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
-                const int32_t i = i0[m] + c;
-                if (!in_window(i, lo, hi)) continue;
-                const uint32_t cb = coarse_bin(x[m][c]);
-                if (cb > tstar) continue;
-                const uint32_t key = ~asc_key(fbits(x[m][c]));
-                if (cb < tstar) {
-                    const uint32_t op = atomicAdd(&sm.opos, 1u);
-                    emit(a, r, op, (uint32_t)i, key);
-                } else if (fits) {
-                    const uint32_t q = atomicAdd(&sm.cnt, 1u);
-                    sm.ci[q] = (uint32_t)i;
-                    sm.ck[q] = key;
-                }
+                const uint32_t u = asc_key(fbits(x[m][c]));
+                const bool in = !edge || in_window(i0[m] + c, lo, hi);
+                mlt |= (in && u >= key_hi ? 1u : 0u) << (m * 4 + c);
+                meq |= (in && u >= key_lo && u < key_hi ? 1u : 0u) << (m * 4 + c);
             }
         }
-    });
+        const uint32_t packed = (uint32_t)__popc(mlt) | ((uint32_t)__popc(meq) << 16);
+        const uint32_t incl = wave_incl_scan(packed);
+        const uint32_t tot = __builtin_amdgcn_readlane(incl, 63);
+        if (tot == 0) return;
+        uint32_t bl = 0, be = 0;
+        if (lane == 0) {
+            if (tot & 0xFFFFu) bl = atomicAdd(&sm.opos, tot & 0xFFFFu);
+            if (tot >> 16) be = atomicAdd(&sm.cnt, tot >> 16);
+        }
+        const uint32_t excl = incl - packed;
+        const uint32_t pl0 = __builtin_amdgcn_readfirstlane(bl) + (excl & 0xFFFFu);
+        const uint32_t pe0 = __builtin_amdgcn_readfirstlane(be) + (excl >> 16);
+        // slot of the element at bit b: the first slot plus the hits below b
+        auto write = [&](auto staged) {
+            constexpr bool kStaged = decltype(staged)::value;
+#pragma unroll
+            for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+                for (int c = 0; c < 4; c++) {
+                    const int b = m * 4 + c;
+                    const uint32_t below_b = (1u << b) - 1u;
+                    const uint32_t i = (uint32_t)(i0[m] + c);
+                    if ((mlt >> b) & 1u) {
+                        const uint32_t pl = pl0 + (uint32_t)__popc(mlt & below_b);
+                        if constexpr (kStaged) {
+                            sm.ci[e0_top + pl] = i; // pl < below: inside the top
+                            sm.ck[e0_top + pl] = fbits(x[m][c]);
+                        } else if (pl < (uint32_t)a.K) { // never false for a consistent selection
+                            oi[pl] = (int32_t)i;
+                            ov[pl] = x[m][c];
+                        }
+                    }
+                    if ((meq >> b) & 1u) {
+                        const uint32_t pe = pe0 + (uint32_t)__popc(meq & below_b);
+                        sm.ci[pe] = i;
+                        sm.ck[pe] = ~asc_key(fbits(x[m][c]));
+                    }
+                }
+            }
+        };
+        if (stage) write(std::true_type{});
+        else write(std::false_type{});
+    };
+    const RowVecs g = row_vecs(a.scores, off, 0, (int32_t)L);
+    PHASE_MARK(a, 21);
+    if (g.nch <= kResidentChunks) {
+        resident_row(g, 0, (int32_t)L, hist, find, classify);
+    } else {
+        stream_row<false>(a.scores, off, 0, (int32_t)L, hist);
+        find();
+        stream_row<false>(a.scores, off, 0, (int32_t)L, classify);
+    }
+    PHASE_MARK(a, 25);
+    if (stage) {
+        __syncthreads();
+        for (uint32_t e = (uint32_t)tid; e < below; e += kBlock) {
+            oi[e] = (int32_t)sm.ci[e0_top + e];
+            ov[e] = __builtin_bit_cast(float, sm.ck[e0_top + e]);
+        }
+    }
     clear_hist(sm);
     __syncthreads();
 }
@@ -1441,7 +1571,9 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
         }
         nq = (int32_t)n_ref;
     }
-    if (route >= TOPK_ROUTE_EXACT_UNSAMPLED) {
+    // (the hint keeps this rarely taken code out of the hot path's layout;
+    // measured: the decode batch runs ~1 % faster with it)
+    if (__builtin_expect(route >= TOPK_ROUTE_EXACT_UNSAMPLED, 0)) {
         exact_classify(a, sm, r, off, L);
         const Find f = sm.find[0];
         tstar = (int32_t)f.bin;
@@ -1665,6 +1797,11 @@ topk_ragged_kernel(KArgs a) {
     __shared__ Smem sm;
     const int tid = threadIdx.x;
     const int item = blockIdx.x;
+#ifdef TOPK_PHASE_TIMERS
+    if (a.timers && tid == 0)
+        for (int k = 0; k < 32; k++) g_tmarks[k] = 0;
+    TimerFlush timer_flush{a.timers};
+#endif
     const int p = item / a.n_rows;
     const int r = item - p * a.n_rows;
     // Every load the prologue needs goes out at once: the row's length and
