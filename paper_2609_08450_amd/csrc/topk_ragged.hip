@@ -1167,25 +1167,54 @@ __device__ __forceinline__ void reread_select(const KArgs a, Smem &sm, int r, in
     __syncthreads();
 }
 
+// Coarse bins of one streamed chunk added into sm.hist.
+__device__ __forceinline__ void coarse_hist_chunk(Smem &sm, const f4 *x, const int32_t *i0,
+                                                  int32_t lo, int32_t hi, bool edge, int32_t mv) {
+#pragma unroll
+    for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+        for (int c = 0; c < 4; c++)
+            if (!edge || in_window(i0[m] + c, lo, hi))
+                atomicAdd(&sm.hist[coarse_bin(x[m][c])], 1u);
+    }
+}
+
+// Coarse histogram of the whole row into sm.hist (clear before a preceding
+// barrier); ends with a barrier.
+__device__ __forceinline__ void exact_hist(const KArgs a, Smem &sm, int64_t off, int64_t L) {
+    stream_row<false>(a.scores, off, 0, (int32_t)L,
+                      [&](const f4 *x, const int32_t *i0, int32_t lo, int32_t hi, bool edge,
+                          int32_t mv) { coarse_hist_chunk(sm, x, i0, lo, hi, edge, mv); });
+    __syncthreads();
+}
+
+// Elements in coarse bins 0..b of the complete histogram in sm.hist, i.e.
+// C(b) (sm.cnt0 zero on entry).  Ends with a barrier.
+__device__ __forceinline__ uint32_t hist_count_upto(Smem &sm, uint32_t b) {
+    const uint32_t t4 = 4u * (uint32_t)threadIdx.x;
+    const uint4 h = reinterpret_cast<const uint4 *>(sm.hist)[threadIdx.x];
+    uint32_t c = (t4 <= b ? h.x : 0u) + (t4 + 1u <= b ? h.y : 0u) + (t4 + 2u <= b ? h.z : 0u) +
+                 (t4 + 3u <= b ? h.w : 0u);
+    c = wave_incl_scan(c);
+    if ((threadIdx.x & 63) == 63 && c) atomicAdd(&sm.cnt0, c);
+    __syncthreads();
+    return sm.cnt0;
+}
+
 // Exact coarse recovery (eq:method:exact-init) over the whole row by this
 // workgroup: a coarse histogram pass finds tau_star = min{b : C(b) >= K}; a
 // classify pass commits c < tau_star to the output (E0) and keeps
 // c == tau_star as the frontier Q0 when it fits the capacity.  A row of at
 // most kResidentChunks chunks is read once and both passes run from
 // registers; a longer one is streamed twice.  Returns (tau_star, |E0|, |Q0|)
-// in sm.find[0]; ends with a barrier, sm.hist cleared.
-__device__ __forceinline__ void exact_classify(const KArgs a, Smem &sm, int r, int64_t off, int64_t L) {
+// in sm.find[0]; ends with a barrier, sm.hist cleared.  With have_hist the
+// coarse histogram is already in sm.hist (exact_hist) and only the classify
+// pass runs.
+__device__ __forceinline__ void exact_classify(const KArgs a, Smem &sm, int r, int64_t off, int64_t L,
+                                               bool have_hist) {
     const int tid = threadIdx.x;
     auto hist = [&](const f4 *x, const int32_t *i0, int32_t lo, int32_t hi, bool edge,
-                    int32_t mv) {
-#pragma unroll
-        for (int m = 0; m < kVec; m++) if (m < mv) {
-#pragma unroll
-            for (int c = 0; c < 4; c++)
-                if (!edge || in_window(i0[m] + c, lo, hi))
-                    atomicAdd(&sm.hist[coarse_bin(x[m][c])], 1u);
-        }
-    };
+                    int32_t mv) { coarse_hist_chunk(sm, x, i0, lo, hi, edge, mv); };
     // After the find: c < tau_star iff u >= key_hi, c == tau_star iff
     // key_lo <= u < key_hi (the bins' ascending-key endpoints); an empty
     // keep range when the bin does not fit the frontier.  When E0 and Q0 fit
@@ -1277,7 +1306,10 @@ __device__ __forceinline__ void exact_classify(const KArgs a, Smem &sm, int r, i
     };
     const RowVecs g = row_vecs(a.scores, off, 0, (int32_t)L);
     PHASE_MARK(a, 21);
-    if (g.nch <= kResidentChunks) {
+    if (have_hist) {
+        find();
+        stream_row<false>(a.scores, off, 0, (int32_t)L, classify);
+    } else if (g.nch <= kResidentChunks) {
         resident_row(g, 0, (int32_t)L, hist, find, classify);
     } else {
         stream_row<false>(a.scores, off, 0, (int32_t)L, hist);
@@ -1525,15 +1557,12 @@ __device__ __forceinline__ bool coop_view_finish(const KArgs a, Smem &sm, int r,
 // tail the route needs.  Also counts the route and writes the trace.
 __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64_t off, int64_t L,
                                            int64_t nv, bool sampled, uint32_t C0, uint32_t C1,
-                                           bool incomplete, bool segmented, uint32_t nstored) {
+                                           bool incomplete, bool segmented, uint32_t nstored,
+                                           bool have_hist = false) {
     const uint32_t K = (uint32_t)a.K;
     const uint32_t cap = (uint32_t)a.cap;
     int32_t trC1 = -1, tstar = -1, nq = -1;
     uint32_t route, n_ref = 0, k_ref = K, kmin = 0;
-    clear_hist(sm);
-    if (threadIdx.x == 0) sm.opos = 0;
-    __syncthreads();
-    PHASE_MARK(a, 8);
     if (!sampled) {
         route = TOPK_ROUTE_EXACT_UNSAMPLED;
     } else if (C0 >= K && C0 <= cap) {
@@ -1552,6 +1581,14 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     } else {
         route = TOPK_ROUTE_EXACT_OVERFLOW;
     }
+    // sm.hist may already hold the row's coarse histogram (have_hist): kept
+    // for the exact route, cleared for the others
+    const bool exact = route >= TOPK_ROUTE_EXACT_UNSAMPLED;
+    have_hist = have_hist && exact;
+    if (!have_hist) clear_hist(sm);
+    if (threadIdx.x == 0) sm.opos = 0;
+    __syncthreads();
+    PHASE_MARK(a, 8);
     // Frontier of the certified tail: A(tau0), or A(tau1) for the band, read
     // from the Phase 2 entries (FP32 bits filtered by kmin) or, when those
     // are incomplete, re-collected from the row as kappa32 keys.
@@ -1573,8 +1610,8 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     }
     // (the hint keeps this rarely taken code out of the hot path's layout;
     // measured: the decode batch runs ~1 % faster with it)
-    if (__builtin_expect(route >= TOPK_ROUTE_EXACT_UNSAMPLED, 0)) {
-        exact_classify(a, sm, r, off, L);
+    if (__builtin_expect(exact, 0)) {
+        exact_classify(a, sm, r, off, L, have_hist);
         const Find f = sm.find[0];
         tstar = (int32_t)f.bin;
         nq = (int32_t)f.eq;
@@ -1857,7 +1894,7 @@ topk_ragged_kernel(KArgs a) {
     uint64_t *gc = reinterpret_cast<uint64_t *>(a.rows + (size_t)r * kRowBlockBytes +
                                                 kRowStateBytes + kViewHistBytes);
     uint32_t C0 = 0, C1 = 0, nstored = 0;
-    bool incomplete = false, segmented = true, split = false;
+    bool incomplete = false, segmented = true, split = false, have_hist = false;
 
     if (sampled) {
         // A row has at most ceil(L / kSegMin) segments (see below).
@@ -1977,9 +2014,20 @@ topk_ragged_kernel(KArgs a) {
                                                         __HIP_MEMORY_SCOPE_AGENT);
         }
         // C(tau0): from the stored A(tau1) entries, or by re-reading this
-        // segment when a wave region overflowed.
-        C0 = incomplete ? count_range(sm, a.scores, off, beg, end, sm.cut0)
-                        : count_tail(sm, sm.cut0);
+        // segment when a wave region overflowed.  A row on one workgroup
+        // re-reads it for the coarse histogram instead, which gives C(tau0)
+        // as well and is the first pass of the exact route, should the row
+        // take it.
+        if (__builtin_expect(incomplete, 0) && !split) {
+            clear_hist(sm);
+            __syncthreads();
+            exact_hist(a, sm, off, L);
+            C0 = hist_count_upto(sm, sm.tau0);
+            have_hist = true;
+        } else {
+            C0 = incomplete ? count_range(sm, a.scores, off, beg, end, sm.cut0)
+                            : count_tail(sm, sm.cut0);
+        }
         PHASE_MARK(a, 2);
         PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)P << 16) | ((uint64_t)r << 32));
 
@@ -2100,7 +2148,7 @@ topk_ragged_kernel(KArgs a) {
         }
         __syncthreads();
     }
-    finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored);
+    finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored, have_hist);
     PHASE_MARK(a, 5);
 
     if (split && tid == 0) reset_row_state(rs);

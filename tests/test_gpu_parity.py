@@ -416,3 +416,30 @@ def test_parity_per_k_policy(topk, K):
     say("routes", st)
     if K >= 4352:
         assert st["primary"] + st["band"] == 0
+
+
+def test_single_workgroup_rows_with_an_overflowed_region(topk):
+    """Rows on one workgroup each (the call has too many rows to split) whose
+    admitted tail lies in positions one wave streams: that wave's region
+    overflows, so C(tau0) comes from the coarse-histogram pass; rows whose
+    proposal certifies re-collect their frontier, overflowing ones reuse the
+    histogram for the exact route."""
+    rng = np.random.default_rng(31)
+    L, n = 24576, 400
+    hot = (np.arange(L) % 2048) < 256   # the positions of wave 0 in every chunk
+    rows = []
+    for i in range(n):
+        x = W.decode_mixture_row(rng, L).astype(np.float32)
+        if i % 4 == 0:                   # C(tau0) within the frontier: primary
+            x[hot] = rng.normal(4.0, 0.1, int(hot.sum())).astype(np.float32)
+        elif i % 4 == 1:                 # the view sees only low values: overflow
+            x[hot] = rng.normal(4.0, 0.1, int(hot.sum())).astype(np.float32)
+            phase = int(format(i % 128, "07b")[::-1], 2)   # the row's view phase
+            x[phase::128] = rng.normal(-2.0, 1.0, x[phase::128].size).astype(np.float32)
+        rows.append(x)
+    lens = np.full(n, L, np.int32)
+    offs = (np.arange(n, dtype=np.int64) * L)
+    wl = W.Workload("one-wave tails", np.concatenate(rows), offs, lens, 2048, "")
+    gt, st = parity(topk, wl)
+    say("routes", st)
+    assert st["primary"] > 0 and st["exact_overflow"] > 0
