@@ -419,6 +419,10 @@ struct NoPrologue {
     __device__ void operator()() const {}
 };
 
+struct NeverStop {
+    __device__ constexpr bool operator()() const { return false; }
+};
+
 // A row range as 16-byte vectors: [beg, end) of the row at element offset
 // off, covered by nvec vectors from vbase (aligned down to 16 bytes; ibase is
 // the row index of vbase's first element), in nch chunks of kChunkVecs.
@@ -472,10 +476,12 @@ __device__ __forceinline__ void consume_chunk(const RowVecs &g, const f4 *src, i
 // Double-buffered chunks: while one chunk (kVec 16-byte loads per thread) is
 // consumed, the next one is in flight.  prologue() runs once, by every
 // thread, with the first chunk in flight (loads it waits for must have been
-// issued before the call, or they would queue behind the chunk).
-template <bool kNT, class F, class Pro = NoPrologue>
+// issued before the call, or they would queue behind the chunk).  A wave
+// leaves the loop after any chunk for which stop() (wave-uniform) holds.
+template <bool kNT, class F, class Pro = NoPrologue, class Stop = NeverStop>
 __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int32_t beg,
-                                           int32_t end, F &&fn, Pro &&prologue = Pro()) {
+                                           int32_t end, F &&fn, Pro &&prologue = Pro(),
+                                           Stop &&stop = Stop()) {
     if (beg >= end) {
         prologue();
         return;
@@ -487,8 +493,10 @@ __device__ __forceinline__ void stream_row(const float *scores, int64_t off, int
     for (int32_t c = 0; c < g.nch; c += 2) {
         issue_chunk<kNT>(g, xb, c + 1);
         consume_chunk(g, xa, c, beg, end, fn);
+        if (stop()) break;
         issue_chunk<kNT>(g, xa, c + 2);
         consume_chunk(g, xb, c + 1, beg, end, fn);
+        if (stop()) break;
     }
 }
 
@@ -562,10 +570,11 @@ __device__ __forceinline__ void collect_range(Smem &sm, const float *scores, int
 // admitted tail.  Every value with ascending key u >= cut1 (the nested
 // boundary, so a C(tau0) < K proposal can take the band of
 // eq:method:rescue-band without a second traversal) is stored as (index, FP32
-// bits) in the private region of its wave: sm.ci/ck[w * kWaveStride ..).  Each element costs one compare; a
-// wave-wide ballot places the hits with no atomics.  C(tau1) and C(tau0) are
-// counted exactly even where a wave region overflows (sm.incomplete is then
-// set).  The endpoints are read from sm after prologue() has run.
+// bits) in the private region of its wave: sm.ci/ck[w * kWaveStride ..).
+// Each element costs one compare; a wave-wide ballot places the hits with no
+// atomics, and sm.cnt gets C(tau1).  A wave whose region overflows sets
+// sm.incomplete and stops (sm.cnt is then partial; the caller re-counts by
+// re-reading).  The endpoints are read from sm after prologue() has run.
 template <class Pro>
 __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, int64_t off,
                                                int32_t beg, int32_t end, Pro &&prologue) {
@@ -622,7 +631,10 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
                 else run(std::false_type{}, std::false_type{});
             }
         },
-        prologue);
+        prologue,
+        // a wave whose region has overflowed stops: the segment's entries
+        // will not be used, and both counts are then taken by a re-read
+        [&]() { return cur > (uint32_t)kWaveCap; });
     if ((threadIdx.x & 63) == 0) {
         sm.wcnt[w] = cur;
         atomicAdd(&sm.cnt, cur);
@@ -652,24 +664,33 @@ __device__ __forceinline__ uint32_t count_tail(Smem &sm, uint32_t kmin) {
     return sm.cnt0;
 }
 
-// C(tau0) of row elements [beg, end) by re-reading them (overflow fallback).
-// sm.cnt0 must be zero on entry.  Ends with a barrier.
-__device__ __forceinline__ uint32_t count_range(Smem &sm, const float *scores, int64_t off,
-                                                int32_t beg, int32_t end, uint32_t kmin) {
-    uint32_t c = 0;
+// C(tau0) and C(tau1) of row elements [beg, end) by re-reading them (after a
+// wave region overflowed), into sm.cnt0 and sm.cnt (zero on entry).  Ends
+// with a barrier.
+__device__ __forceinline__ void count_range(Smem &sm, const float *scores, int64_t off,
+                                            int32_t beg, int32_t end, uint32_t cut0,
+                                            uint32_t cut1) {
+    uint32_t c0 = 0, c1 = 0;
     stream_row<false>(scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
                                                  int32_t hi, bool, int32_t mv) {
 #pragma unroll
         for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
-            for (int cc = 0; cc < 4; cc++)
-                c += (in_window(i0[m] + cc, lo, hi) && asc_key(fbits(x[m][cc])) >= kmin) ? 1u : 0u;
+            for (int cc = 0; cc < 4; cc++) {
+                const uint32_t u = asc_key(fbits(x[m][cc]));
+                const bool in = in_window(i0[m] + cc, lo, hi);
+                c0 += (in && u >= cut0) ? 1u : 0u;
+                c1 += (in && u >= cut1) ? 1u : 0u;
+            }
         }
     });
-    c = wave_incl_scan(c);
-    if ((threadIdx.x & 63) == 63 && c) atomicAdd(&sm.cnt0, c);
+    c0 = wave_incl_scan(c0);
+    c1 = wave_incl_scan(c1);
+    if ((threadIdx.x & 63) == 63) {
+        if (c0) atomicAdd(&sm.cnt0, c0);
+        if (c1) atomicAdd(&sm.cnt, c1);
+    }
     __syncthreads();
-    return sm.cnt0;
 }
 
 // ----------------------------------------------------------- outputs ----
@@ -1188,17 +1209,23 @@ __device__ __forceinline__ void exact_hist(const KArgs a, Smem &sm, int64_t off,
     __syncthreads();
 }
 
-// Elements in coarse bins 0..b of the complete histogram in sm.hist, i.e.
-// C(b) (sm.cnt0 zero on entry).  Ends with a barrier.
-__device__ __forceinline__ uint32_t hist_count_upto(Smem &sm, uint32_t b) {
+// C(b0) and C(b1) from the complete coarse histogram in sm.hist (elements
+// in bins 0..b), into sm.cnt0 and sm.cnt (zero on entry).  Ends with a
+// barrier.
+__device__ __forceinline__ void hist_counts(Smem &sm, uint32_t b0, uint32_t b1) {
     const uint32_t t4 = 4u * (uint32_t)threadIdx.x;
     const uint4 h = reinterpret_cast<const uint4 *>(sm.hist)[threadIdx.x];
-    uint32_t c = (t4 <= b ? h.x : 0u) + (t4 + 1u <= b ? h.y : 0u) + (t4 + 2u <= b ? h.z : 0u) +
-                 (t4 + 3u <= b ? h.w : 0u);
-    c = wave_incl_scan(c);
-    if ((threadIdx.x & 63) == 63 && c) atomicAdd(&sm.cnt0, c);
+    auto upto = [&](uint32_t b) {
+        return (t4 <= b ? h.x : 0u) + (t4 + 1u <= b ? h.y : 0u) + (t4 + 2u <= b ? h.z : 0u) +
+               (t4 + 3u <= b ? h.w : 0u);
+    };
+    const uint32_t c0 = wave_incl_scan(upto(b0));
+    const uint32_t c1 = wave_incl_scan(upto(b1));
+    if ((threadIdx.x & 63) == 63) {
+        if (c0) atomicAdd(&sm.cnt0, c0);
+        if (c1) atomicAdd(&sm.cnt, c1);
+    }
     __syncthreads();
-    return sm.cnt0;
 }
 
 // Exact coarse recovery (eq:method:exact-init) over the whole row by this
@@ -2013,20 +2040,27 @@ topk_ragged_kernel(KArgs a) {
                 resv = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)nst, __ATOMIC_RELAXED,
                                                         __HIP_MEMORY_SCOPE_AGENT);
         }
-        // C(tau0): from the stored A(tau1) entries, or by re-reading this
-        // segment when a wave region overflowed.  A row on one workgroup
-        // re-reads it for the coarse histogram instead, which gives C(tau0)
-        // as well and is the first pass of the exact route, should the row
-        // take it.
-        if (__builtin_expect(incomplete, 0) && !split) {
-            clear_hist(sm);
+        // C(tau0): from the stored A(tau1) entries.  When a wave region
+        // overflowed (that wave stopped early), C(tau0) and C(tau1) are
+        // counted by re-reading this segment; a row on one workgroup re-reads
+        // it for the coarse histogram instead, which gives both counts and is
+        // the first pass of the exact route, should the row take it.
+        if (__builtin_expect(incomplete, 0)) {
+            __syncthreads(); // every thread has read sm.cnt
+            if (tid == 0) sm.cnt = 0; // (sm.cnt0 is still zero)
+            if (!split) clear_hist(sm);
             __syncthreads();
-            exact_hist(a, sm, off, L);
-            C0 = hist_count_upto(sm, sm.tau0);
-            have_hist = true;
+            if (!split) {
+                exact_hist(a, sm, off, L);
+                hist_counts(sm, sm.tau0, sm.tau1);
+                have_hist = true;
+            } else {
+                count_range(sm, a.scores, off, beg, end, sm.cut0, sm.cut1);
+            }
+            C0 = sm.cnt0;
+            C1 = sm.cnt;
         } else {
-            C0 = incomplete ? count_range(sm, a.scores, off, beg, end, sm.cut0)
-                            : count_tail(sm, sm.cut0);
+            C0 = count_tail(sm, sm.cut0);
         }
         PHASE_MARK(a, 2);
         PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)P << 16) | ((uint64_t)r << 32));
