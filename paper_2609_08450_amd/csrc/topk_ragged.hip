@@ -1755,7 +1755,7 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
             }
         }
     }
-    if (tid == 0) sm.knext = 0u;
+    if (tid == 0) { sm.knext = 0u; sm.opos = 0u; }
     __syncthreads();
     PHASE_MARK(a, 9);
     // every wave locates the boundary bin itself (no second barrier)
@@ -1776,16 +1776,16 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
     const uint32_t ce = min(cb + (((uint32_t)1 << win.wf) - 1u), win.kspan);
     const uint32_t cend = take_all ? ce + 1u : cb;
     const uint32_t kw = ce - cb; // keep iff tl - cb <= kw (never for ~0: ce < ~0)
+    // each wave reserves its committed slots with one LDS atomic (slot order
+    // is free: the outputs are a set), so no barrier is needed before placing
     uint32_t cw = 0;
 #pragma unroll
     for (int j = 0; j < kPer; j++)
         if ((uint32_t)j < ngroups) cw += (uint32_t)__popcll(__ballot(tl[j] < cend));
-    if (lane == 0) sm.wc[w8] = cw;
-    __syncthreads();
-    PHASE_MARK(a, 11);
     uint32_t cbase = 0;
-#pragma unroll
-    for (uint32_t v = 0; v < (uint32_t)kWaves; v++) cbase += v < w8 ? sm.wc[v] : 0u;
+    if (lane == 0 && cw) cbase = atomicAdd(&sm.opos, cw);
+    cbase = __builtin_amdgcn_readfirstlane(cbase);
+    PHASE_MARK(a, 11);
     const int64_t out0 = (int64_t)r * a.K;
     uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
     // committed entries are staged in sm.ci/ck[0, K) (free in this path: the
