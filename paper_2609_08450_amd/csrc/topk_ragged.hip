@@ -75,9 +75,8 @@ struct RowState {
     uint64_t sa;         // entries reserved in the candidate buffer (low 32
                          // bits) | segments done with Phase 2 << 32: the last
                          // arrival's atomic returns the final reserved count
+    uint64_t counts;     // C(tau1) | C(tau0) << 32 of the row (exact)
     uint32_t taus;       // segment 0's tau0 | tau1 << 16 | 1 << 31 once known
-    uint32_t count1;     // C(tau1) of the row (exact)
-    uint32_t count0;     // C(tau0) of the row (exact)
     uint32_t incomplete; // a segment could not keep all of its A(tau1)
     uint32_t amax;       // largest ascending key among the stored entries
     uint32_t varrive;    // segments that have added their part of a shared view
@@ -1847,8 +1846,7 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
 
 // Leaves a split row's state zeroed for the next call (graph replays).
 __device__ __forceinline__ void reset_row_state(RowState *rs) {
-    __hip_atomic_store(&rs->count1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&rs->count0, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->counts, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->sa, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2022,63 +2020,97 @@ topk_ragged_kernel(KArgs a) {
         incomplete = sm.incomplete != 0;
         // Split rows publish this segment's entries and counts
         // (eq:method:split-local), then arrive; the last arrival merges them
-        // (eq:method:split-reduce) and finishes the row.  The segment's slots
-        // in the row's merged array are reserved first, so that the atomic's
-        // round trip overlaps the C(tau0) count.
-        // this wave's stored entries, those of the waves before it, all
-        const uint32_t w8 = (uint32_t)tid >> 6;
-        uint32_t wcnt = 0, wpre = 0, nst = 0, resv = 0;
-        if (split) {
-#pragma unroll
-            for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
-                const uint32_t c = min(sm.wcnt[v], (uint32_t)kWaveCap);
-                wcnt = v == w8 ? c : wcnt;
-                wpre += v < w8 ? c : 0u;
-                nst += c;
-            }
-            if (tid == 0 && nst)
-                resv = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)nst, __ATOMIC_RELAXED,
+        // (eq:method:split-reduce) and finishes the row.  With every region
+        // complete each wave publishes its own part: it reserves slots for
+        // its entries in the row's merged array (the atomic's round trip
+        // overlaps its count of C(tau0)), adds its two counts in one 64-bit
+        // atomic and its maximum, and copies its region; no barrier is needed
+        // until the arrival.  Otherwise the block counts first (see below).
+        const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
+        uint32_t wcnt = 0, dst = 0; // this wave's stored entries, and their first slot
+        if (split && !incomplete) {
+            wcnt = sm.wcnt[w8];
+            uint32_t wres = 0;
+            if (lane == 0 && wcnt)
+                wres = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)wcnt, __ATOMIC_RELAXED,
                                                         __HIP_MEMORY_SCOPE_AGENT);
-        }
-        // C(tau0): from the stored A(tau1) entries.  When a wave region
-        // overflowed (that wave stopped early), C(tau0) and C(tau1) are
-        // counted by re-reading this segment; a row on one workgroup re-reads
-        // it for the coarse histogram instead, which gives both counts and is
-        // the first pass of the exact route, should the row take it.
-        if (__builtin_expect(incomplete, 0)) {
-            __syncthreads(); // every thread has read sm.cnt
-            if (tid == 0) sm.cnt = 0; // (sm.cnt0 is still zero)
-            if (!split) clear_hist(sm);
-            __syncthreads();
-            if (!split) {
-                exact_hist(a, sm, off, L);
-                hist_counts(sm, sm.tau0, sm.tau1);
-                have_hist = true;
-            } else {
-                count_range(sm, a.scores, off, beg, end, sm.cut0, sm.cut1);
+            const uint32_t beg_e = w8 * kWaveStride, end_e = beg_e + wcnt;
+            uint32_t c = 0, mx = 0;
+            for (uint32_t e = beg_e + lane; e < end_e; e += 64) {
+                const uint32_t u = asc_key(sm.ck[e]);
+                c += u >= sm.cut0 ? 1u : 0u;
+                mx = max(mx, u);
             }
-            C0 = sm.cnt0;
-            C1 = sm.cnt;
+            c = __builtin_amdgcn_readlane(wave_incl_scan(c), 63);
+            mx = __builtin_amdgcn_readlane(wave_max_to63(mx), 63);
+            if (lane == 0 && wcnt) {
+                __hip_atomic_fetch_add(&rs->counts, (uint64_t)wcnt | ((uint64_t)c << 32),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_max(&rs->amax, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            dst = __builtin_amdgcn_readfirstlane(wres);
+            PHASE_MARK(a, 2);
         } else {
-            C0 = count_tail(sm, sm.cut0);
+            uint32_t wpre = 0, nst = 0, resv = 0;
+            if (split) {
+#pragma unroll
+                for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
+                    const uint32_t cv = min(sm.wcnt[v], (uint32_t)kWaveCap);
+                    wcnt = v == w8 ? cv : wcnt;
+                    wpre += v < w8 ? cv : 0u;
+                    nst += cv;
+                }
+                if (tid == 0 && nst)
+                    resv = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)nst,
+                                                            __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT);
+            }
+            // C(tau0): from the stored A(tau1) entries.  When a wave region
+            // overflowed (that wave stopped early), C(tau0) and C(tau1) are
+            // counted by re-reading this segment; a row on one workgroup
+            // re-reads it for the coarse histogram instead, which gives both
+            // counts and is the first pass of the exact route, should the row
+            // take it.
+            if (__builtin_expect(incomplete, 0)) {
+                __syncthreads(); // every thread has read sm.cnt
+                if (tid == 0) sm.cnt = 0; // (sm.cnt0 is still zero)
+                if (!split) clear_hist(sm);
+                __syncthreads();
+                if (!split) {
+                    exact_hist(a, sm, off, L);
+                    hist_counts(sm, sm.tau0, sm.tau1);
+                    have_hist = true;
+                } else {
+                    count_range(sm, a.scores, off, beg, end, sm.cut0, sm.cut1);
+                }
+                C0 = sm.cnt0;
+                C1 = sm.cnt;
+            } else {
+                C0 = count_tail(sm, sm.cut0);
+            }
+            PHASE_MARK(a, 2);
+            if (split) {
+                if (tid == 0) {
+                    sm.base = resv;
+                    if (C1 | C0)
+                        __hip_atomic_fetch_add(&rs->counts, (uint64_t)C1 | ((uint64_t)C0 << 32),
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (incomplete)
+                        __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                    else if (nst)
+                        __hip_atomic_fetch_max(&rs->amax, sm.amax, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                }
+                __syncthreads();
+                dst = sm.base + wpre;
+            }
         }
-        PHASE_MARK(a, 2);
         PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)P << 16) | ((uint64_t)r << 32));
 
         if (split) {
-            if (tid == 0) {
-                sm.base = resv;
-                if (C1) __hip_atomic_fetch_add(&rs->count1, C1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (C0) __hip_atomic_fetch_add(&rs->count0, C0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (incomplete)
-                    __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                else if (nst)
-                    __hip_atomic_fetch_max(&rs->amax, sm.amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            __syncthreads();
             // each wave copies its own region, consecutive slots
-            const uint32_t dst = sm.base + wpre;
-            for (uint32_t e = (uint32_t)lane_id(); e < wcnt; e += 64) {
+            for (uint32_t e = lane; e < wcnt; e += 64) {
                 const uint32_t d = dst + e;
                 const uint32_t t = w8 * kWaveStride + e;
                 if (d < (uint32_t)kFront)
@@ -2110,8 +2142,10 @@ topk_ragged_kernel(KArgs a) {
             const uint32_t stored = sm.base;
             const uint32_t ngroups = (min(stored, (uint32_t)kFront) + kBlock - 1) / kBlock;
             if (tid == 0) {
-                sm.cnt = __hip_atomic_load(&rs->count1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                sm.cnt0 = __hip_atomic_load(&rs->count0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint64_t cc = __hip_atomic_load(&rs->counts, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+                sm.cnt = (uint32_t)cc;
+                sm.cnt0 = (uint32_t)(cc >> 32);
                 sm.incomplete = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 sm.amax = __hip_atomic_load(&rs->amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
