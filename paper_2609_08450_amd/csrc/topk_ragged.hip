@@ -2117,6 +2117,9 @@ topk_ragged_kernel(KArgs a) {
                     __hip_atomic_store(&gc[d], ((uint64_t)sm.ck[t] << 32) | sm.ci[t],
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            // (the histogram is cleared for the finisher's use while the
+            // copies complete)
+            clear_hist(sm);
             // Every value another workgroup reads (entries, counts, the
             // arrival counter) is an agent-scope atomic access, which the
             // hardware keeps coherent across the XCDs' L2 caches without a
@@ -2138,16 +2141,18 @@ topk_ragged_kernel(KArgs a) {
             // Finisher (its sm.cut0, cut1, tau0, tau1 are the row's endpoints).
             // The counts and the slot groups that hold candidates are loaded
             // in one round trip (slots past the stored count in the last
-            // group hold stale words, ignored), all as agent-scope atomics.
+            // group hold stale words, ignored), all as agent-scope atomics;
+            // each wave loads the counts itself, so no barrier follows.
             const uint32_t stored = sm.base;
             const uint32_t ngroups = (min(stored, (uint32_t)kFront) + kBlock - 1) / kBlock;
-            if (tid == 0) {
+            uint32_t c1 = 0, c0 = 0, inc = 0, amx = 0;
+            if (lane == 0) {
                 const uint64_t cc = __hip_atomic_load(&rs->counts, __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT);
-                sm.cnt = (uint32_t)cc;
-                sm.cnt0 = (uint32_t)(cc >> 32);
-                sm.incomplete = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                sm.amax = __hip_atomic_load(&rs->amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                c1 = (uint32_t)cc;
+                c0 = (uint32_t)(cc >> 32);
+                inc = __hip_atomic_load(&rs->incomplete, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                amx = __hip_atomic_load(&rs->amax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             uint32_t vi[kPer], vk[kPer];
 #pragma unroll
@@ -2159,16 +2164,16 @@ topk_ragged_kernel(KArgs a) {
                 vi[j] = (uint32_t)v;
                 vk[j] = (uint32_t)(v >> 32);
             }
-            clear_hist(sm);
-            __syncthreads();
-            C1 = sm.cnt;
-            C0 = sm.cnt0;
-            incomplete = sm.incomplete != 0 || stored > (uint32_t)kFront;
+            C1 = __builtin_amdgcn_readfirstlane(c1);
+            C0 = __builtin_amdgcn_readfirstlane(c0);
+            amx = __builtin_amdgcn_readfirstlane(amx);
+            incomplete = __builtin_amdgcn_readfirstlane(inc) != 0 || stored > (uint32_t)kFront;
+            if (tid == 0) sm.amax = amx; // for the general finish (barriers follow)
             nstored = incomplete ? 0u : stored;
             segmented = false;
             PHASE_MARK(a, 4);
             if (!incomplete &&
-                finish_fast(a, sm, r, nv, C0, C1, sm.amax, kBlock, (uint32_t)tid, nstored,
+                finish_fast(a, sm, r, nv, C0, C1, amx, kBlock, (uint32_t)tid, nstored,
                             ngroups, vi, vk)) {
                 PHASE_MARK(a, 5);
                 if (tid == 0) reset_row_state(rs);
