@@ -1402,7 +1402,8 @@ __device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm, i
 // than kP1 * kBlock), finds tau0 and tau1 and their FP32 endpoints
 // (eq:method:sample-hist, eq:method:primary-threshold) into sm.  Every
 // segment of a split row computes the same view (no cross-workgroup wait).
-// sm.hist must have been cleared before a barrier preceding phase1_finish.
+// sm.hist must have been cleared, before a barrier preceding phase1_finish
+// when synced, else before the call.
 constexpr int kP1 = 16;
 
 __device__ __forceinline__ void phase1_issue(const KArgs a, int r, const float *row, int64_t L,
@@ -1421,11 +1422,12 @@ __device__ __forceinline__ void phase1_issue(const KArgs a, int r, const float *
 // pub (segment 0 of a split row): where tau0 | tau1 << 16 | 1 << 31 is
 // published for the other segments, as soon as it is known.
 __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, const float *row,
-                                              int64_t L, const float (&xs)[kP1], uint32_t *pub) {
+                                              int64_t L, const float (&xs)[kP1], uint32_t *pub,
+                                              bool synced) {
     const int tid = threadIdx.x;
     const uint32_t ph = view_phase(r, a.s_log2);
     const int64_t nv = view_size(L, ph, a.s_log2);
-    __syncthreads();
+    if (!synced) __syncthreads(); // the clear of sm.hist before the additions
     PHASE_MARK(a, 17);
     // bin counts, and their sums over groups of 32 bins for a two-level find
     auto add = [&](float x) {
@@ -1980,7 +1982,8 @@ topk_ragged_kernel(KArgs a) {
             if (coop) {
                 have = coop_view_finish(a, sm, r, row, k0, k1, xs, rs, vh, P);
             } else if (p == 0) {
-                phase1_finish(a, sm, r, row, L, xs, split ? &rs->taus : nullptr);
+                // (a split plan's length sum ended with a barrier)
+                phase1_finish(a, sm, r, row, L, xs, split ? &rs->taus : nullptr, a.pmax > 1);
                 have = true;
             }
             if (!have) {
@@ -2010,7 +2013,7 @@ topk_ragged_kernel(KArgs a) {
                     clear_hist(sm);
                     __syncthreads();
                     phase1_issue(a, r, row, L, xs);
-                    phase1_finish(a, sm, r, row, L, xs, nullptr);
+                    phase1_finish(a, sm, r, row, L, xs, nullptr, true);
                 }
             }
             PHASE_MARK(a, 1);
