@@ -443,3 +443,30 @@ def test_single_workgroup_rows_with_an_overflowed_region(topk):
     gt, st = parity(topk, wl)
     say("routes", st)
     assert st["primary"] > 0 and st["exact_overflow"] > 0
+
+
+def test_split_rows_with_an_overflowed_region(topk):
+    """Rows split across workgroups (a call of 48 rows) where some segments
+    see their admitted tail in one wave's positions: those segments re-count
+    by re-reading (both counts), the others publish per wave, and the
+    finisher of a row with an incomplete segment re-collects or takes the
+    exact route."""
+    rng = np.random.default_rng(37)
+    n = 48
+    lens = rng.integers(40000, 131072, n).astype(np.int32)
+    rows = []
+    for i, L in enumerate(lens):
+        x = W.decode_mixture_row(rng, int(L)).astype(np.float32)
+        hot = np.nonzero((np.arange(L) % 2048) < 256)[0]
+        if i % 3 == 0:      # a tail of ~2.5 K in wave-0 positions of one stretch
+            sel = hot[(hot > L // 3) & (hot < L // 3 + 20000)]
+            x[sel] = rng.normal(4.0, 0.1, sel.size).astype(np.float32)
+        elif i % 3 == 1:    # too many candidates everywhere: overflow
+            phase = int(format(i % 128, "07b")[::-1], 2)
+            x[phase::128] = rng.normal(-2.0, 1.0, x[phase::128].size).astype(np.float32)
+        rows.append(x)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload("split one-wave tails", np.concatenate(rows), offs, lens, 2048, "")
+    gt, st = parity(topk, wl)
+    say("routes", st)
+    assert st["exact_overflow"] > 0 and st["primary"] + st["band"] > 0
