@@ -62,6 +62,8 @@ constexpr size_t kRowBlockBytes = kRowStateBytes + kViewHistBytes + 2 * kFront *
 // merged): one workgroup gathering them all is bound by its cache-line
 // fills (one 128-byte line per 4-byte sample).
 constexpr int64_t kCoopView = 4096;
+// Most segments a row may have for its segments to publish per wave.
+constexpr int64_t kWavePublishMaxSegs = 16;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -2028,10 +2030,12 @@ topk_ragged_kernel(KArgs a) {
         // its entries in the row's merged array (the atomic's round trip
         // overlaps its count of C(tau0)), adds its two counts in one 64-bit
         // atomic and its maximum, and copies its region; no barrier is needed
-        // until the arrival.  Otherwise the block counts first (see below).
+        // until the arrival.  Otherwise, or when the row has many segments
+        // (whose per-wave atomics on the same words would queue), the block
+        // counts first (see below).
         const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
         uint32_t wcnt = 0, dst = 0; // this wave's stored entries, and their first slot
-        if (split && !incomplete) {
+        if (split && !incomplete && P <= kWavePublishMaxSegs) {
             wcnt = sm.wcnt[w8];
             uint32_t wres = 0;
             if (lane == 0 && wcnt)
