@@ -665,12 +665,10 @@ __device__ __forceinline__ uint32_t count_tail(Smem &sm, uint32_t kmin) {
     return sm.cnt0;
 }
 
-// C(tau0) and C(tau1) of row elements [beg, end) by re-reading them (after a
-// wave region overflowed), into sm.cnt0 and sm.cnt (zero on entry).  Ends
-// with a barrier.
-__device__ __forceinline__ void count_range(Smem &sm, const float *scores, int64_t off,
-                                            int32_t beg, int32_t end, uint32_t cut0,
-                                            uint32_t cut1) {
+// C(tau0) and C(tau1) (.x, .y, wave-uniform) of the row elements [beg, end)
+// that this wave's lanes stream (stream_row's positions of these threads).
+__device__ __forceinline__ uint2 count_range_wave(const float *scores, int64_t off, int32_t beg,
+                                                  int32_t end, uint32_t cut0, uint32_t cut1) {
     uint32_t c0 = 0, c1 = 0;
     stream_row<false>(scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
                                                  int32_t hi, bool, int32_t mv) {
@@ -685,11 +683,20 @@ __device__ __forceinline__ void count_range(Smem &sm, const float *scores, int64
             }
         }
     });
-    c0 = wave_incl_scan(c0);
-    c1 = wave_incl_scan(c1);
-    if ((threadIdx.x & 63) == 63) {
-        if (c0) atomicAdd(&sm.cnt0, c0);
-        if (c1) atomicAdd(&sm.cnt, c1);
+    return make_uint2(__builtin_amdgcn_readlane(wave_incl_scan(c0), 63),
+                      __builtin_amdgcn_readlane(wave_incl_scan(c1), 63));
+}
+
+// C(tau0) and C(tau1) of row elements [beg, end) by re-reading them (after a
+// wave region overflowed), into sm.cnt0 and sm.cnt (zero on entry).  Ends
+// with a barrier.
+__device__ __forceinline__ void count_range(Smem &sm, const float *scores, int64_t off,
+                                            int32_t beg, int32_t end, uint32_t cut0,
+                                            uint32_t cut1) {
+    const uint2 c = count_range_wave(scores, off, beg, end, cut0, cut1);
+    if ((threadIdx.x & 63) == 0) {
+        if (c.x) atomicAdd(&sm.cnt0, c.x);
+        if (c.y) atomicAdd(&sm.cnt, c.y);
     }
     __syncthreads();
 }
@@ -2020,44 +2027,61 @@ topk_ragged_kernel(KArgs a) {
             }
             PHASE_MARK(a, 1);
         });
-        __syncthreads();
-        C1 = sm.cnt;
-        incomplete = sm.incomplete != 0;
         // Split rows publish this segment's entries and counts
         // (eq:method:split-local), then arrive; the last arrival merges them
-        // (eq:method:split-reduce) and finishes the row.  With every region
-        // complete each wave publishes its own part: it reserves slots for
-        // its entries in the row's merged array (the atomic's round trip
-        // overlaps its count of C(tau0)), adds its two counts in one 64-bit
-        // atomic and its maximum, and copies its region; no barrier is needed
-        // until the arrival.  Otherwise, or when the row has many segments
-        // (whose per-wave atomics on the same words would queue), the block
-        // counts first (see below).
+        // (eq:method:split-reduce) and finishes the row.  When the row has few
+        // segments each wave publishes on its own, with no workgroup barrier
+        // before the arrival: it reserves slots for its entries in the row's
+        // merged array (the atomic's round trip overlaps its count of
+        // C(tau0)), adds its two counts in one 64-bit atomic and its maximum,
+        // and copies its region; a wave whose region overflowed re-counts the
+        // positions it streams and marks the row incomplete.  With many
+        // segments (whose per-wave atomics on the same words would queue) the
+        // workgroup counts and publishes as one.  Either way the workgroup
+        // arrives once.
         const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
+        const bool wave_publish = split && P <= kWavePublishMaxSegs;
         uint32_t wcnt = 0, dst = 0; // this wave's stored entries, and their first slot
-        if (split && !incomplete && P <= kWavePublishMaxSegs) {
-            wcnt = sm.wcnt[w8];
-            uint32_t wres = 0;
-            if (lane == 0 && wcnt)
-                wres = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)wcnt, __ATOMIC_RELAXED,
-                                                        __HIP_MEMORY_SCOPE_AGENT);
-            const uint32_t beg_e = w8 * kWaveStride, end_e = beg_e + wcnt;
-            uint32_t c = 0, mx = 0;
-            for (uint32_t e = beg_e + lane; e < end_e; e += 64) {
-                const uint32_t u = asc_key(sm.ck[e]);
-                c += u >= sm.cut0 ? 1u : 0u;
-                mx = max(mx, u);
+        if (wave_publish) {
+            const uint32_t cur_w = sm.wcnt[w8]; // this wave's own count
+            if (cur_w <= (uint32_t)kWaveCap) {
+                wcnt = cur_w;
+                uint32_t wres = 0;
+                if (lane == 0 && wcnt)
+                    wres = (uint32_t)__hip_atomic_fetch_add(&rs->sa, (uint64_t)wcnt,
+                                                            __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t beg_e = w8 * kWaveStride, end_e = beg_e + wcnt;
+                uint32_t c = 0, mx = 0;
+                for (uint32_t e = beg_e + lane; e < end_e; e += 64) {
+                    const uint32_t u = asc_key(sm.ck[e]);
+                    c += u >= sm.cut0 ? 1u : 0u;
+                    mx = max(mx, u);
+                }
+                c = __builtin_amdgcn_readlane(wave_incl_scan(c), 63);
+                mx = __builtin_amdgcn_readlane(wave_max_to63(mx), 63);
+                if (lane == 0 && wcnt) {
+                    __hip_atomic_fetch_add(&rs->counts, (uint64_t)wcnt | ((uint64_t)c << 32),
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_fetch_max(&rs->amax, mx, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                }
+                dst = __builtin_amdgcn_readfirstlane(wres);
+            } else {
+                const uint2 cc = count_range_wave(a.scores, off, beg, end, sm.cut0, sm.cut1);
+                if (lane == 0) {
+                    if (cc.x | cc.y)
+                        __hip_atomic_fetch_add(&rs->counts, (uint64_t)cc.y | ((uint64_t)cc.x << 32),
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                }
             }
-            c = __builtin_amdgcn_readlane(wave_incl_scan(c), 63);
-            mx = __builtin_amdgcn_readlane(wave_max_to63(mx), 63);
-            if (lane == 0 && wcnt) {
-                __hip_atomic_fetch_add(&rs->counts, (uint64_t)wcnt | ((uint64_t)c << 32),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_fetch_max(&rs->amax, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            dst = __builtin_amdgcn_readfirstlane(wres);
             PHASE_MARK(a, 2);
         } else {
+            __syncthreads();
+            C1 = sm.cnt;
+            incomplete = sm.incomplete != 0;
             uint32_t wpre = 0, nst = 0, resv = 0;
             if (split) {
 #pragma unroll
