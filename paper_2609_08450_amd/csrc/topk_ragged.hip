@@ -335,6 +335,26 @@ __device__ __forceinline__ Find wave_find_reg(const uint32_t *hist, uint32_t inc
     return f;
 }
 
+// wave_find_reg for two targets at once (bins only): both owner groups are
+// read from LDS together, so the two searches share their latencies.
+__device__ __forceinline__ void wave_find_bins2(const uint32_t *hist, uint32_t incl, uint32_t tot,
+                                                uint32_t total, uint32_t k0, uint32_t k1,
+                                                uint32_t &b0, uint32_t &b1) {
+    const int lane = lane_id();
+    const bool ok0 = k0 != 0 && k0 <= total, ok1 = k1 != 0 && k1 <= total;
+    const int own0 = ok0 ? __ffsll((unsigned long long)__ballot(incl >= k0)) - 1 : 0;
+    const int own1 = ok1 ? __ffsll((unsigned long long)__ballot(incl >= k1)) - 1 : 0;
+    const uint32_t base0 = __builtin_amdgcn_readlane(incl - tot, own0);
+    const uint32_t base1 = __builtin_amdgcn_readlane(incl - tot, own1);
+    const uint32_t v0 = (lane < 32) ? hist[own0 * 32 + lane] : 0u;
+    const uint32_t v1 = (lane < 32) ? hist[own1 * 32 + lane] : 0u;
+    const uint32_t i0 = wave_incl_scan(v0), i1 = wave_incl_scan(v1);
+    const int l0 = __ffsll((unsigned long long)__ballot(lane < 32 && base0 + i0 >= k0)) - 1;
+    const int l1 = __ffsll((unsigned long long)__ballot(lane < 32 && base1 + i1 >= k1)) - 1;
+    b0 = ok0 ? (uint32_t)(own0 * 32 + l0) : (uint32_t)kBins;
+    b1 = ok1 ? (uint32_t)(own1 * 32 + l1) : (uint32_t)kBins;
+}
+
 __device__ __forceinline__ void wave_find(const uint32_t *hist, uint32_t k0, uint32_t k1, int nk, Find *out) {
     const int lane = lane_id();
     const uint4 *h4 = reinterpret_cast<const uint4 *>(hist + lane * 32);
@@ -1472,8 +1492,8 @@ __device__ __forceinline__ void phase1_finish(const KArgs a, Smem &sm, int r, co
         const uint32_t c = sm.coarse[0][lane_id()];
         const uint32_t incl = wave_incl_scan(c);
         const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
-        const uint32_t t0 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q0).bin;
-        const uint32_t t1 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q1).bin;
+        uint32_t t0, t1;
+        wave_find_bins2(sm.hist, incl, c, total, (uint32_t)a.q0, (uint32_t)a.q1, t0, t1);
         if (tid == 0 && pub)
             __hip_atomic_store(pub, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
@@ -1565,8 +1585,8 @@ __device__ __forceinline__ bool coop_view_finish(const KArgs a, Smem &sm, int r,
         const uint32_t c = sm.coarse[0][lane_id()];
         const uint32_t incl = wave_incl_scan(c);
         const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
-        const uint32_t t0 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q0).bin;
-        const uint32_t t1 = wave_find_reg(sm.hist, incl, c, total, (uint32_t)a.q1).bin;
+        uint32_t t0, t1;
+        wave_find_bins2(sm.hist, incl, c, total, (uint32_t)a.q0, (uint32_t)a.q1, t0, t1);
         if (tid == 0)
             __hip_atomic_store(&rs->taus, t0 | (t1 << 16) | 0x80000000u, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
