@@ -241,7 +241,7 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0):
     return ms / steps, routes, copies, G, wreps * G
 
 
-ABLATIONS = ("margin", "stride", "rescue", "crossover", "k", "recal", "recal-crossover")
+ABLATIONS = ("margin", "stride", "rescue", "crossover", "k", "recal", "recal-crossover", "batch")
 
 
 def ablation(name, wl, steps, warmup):
@@ -297,6 +297,9 @@ def ablation(name, wl, steps, warmup):
                                      with_k(wl, K),
                                      pol(s_log2=sl, rho_num=rn, rho_den=rd, rho1_num=r1n,
                                          rho1_den=r1d)))
+    elif name == "batch":     # decode rows, more of them: where the latency chain amortises
+        for n in (16, 32, 64, 128, 256, 512, 1024):
+            variants.append((f"rows={n}", W.decode(n_rows=n), None))
     elif name == "recal-crossover":  # per-K policy: sampled against exact on short rows
         for K in (256, 512, 1024, 2048, 4096):
             kp = topk.policy_for_k(K).as_dict()
@@ -317,7 +320,9 @@ def ablation(name, wl, steps, warmup):
         print(json.dumps({"ablation": name, "variant": label, "rows": w.n_rows, "K": w.K,
                           "us_per_call": round(ms * 1e3, 3),
                           "gbs": round(4.0 * w.total_len / (ms * 1e-3) / 1e9, 2),
-                          "routes": routes, "policy": p.as_dict()}), flush=True)
+                          "routes": routes,
+                          "policy": (p if p is not None else topk.policy_for_k(w.K)).as_dict()}),
+              flush=True)
 
 
 def main():

@@ -1971,7 +1971,10 @@ topk_ragged_kernel(KArgs a) {
         int64_t P = 1, seg = L;
         if (a.pmax > 1) {
             const int64_t total = block_total_length(a, sm, tid < a.n_rows ? len0_raw : 0);
-            const int64_t items = a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
+            // (a call of more rows than items cuts only the rows longer than
+            // the mean, in two: the longest rows no longer bound the call)
+            const int64_t items = a.n_rows > a.seg_items ? a.n_rows
+                                : a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
                                                              : (a.seg_items + 1) / 2;
             // Divisions in FP64 (a few instructions, where 64-bit integer
             // division takes hundreds).  target and P0 may be off by one
@@ -2351,12 +2354,16 @@ int32_t plan_items(int cus) {
 
 // Most segments per row: a power of two in [1, kMaxSplit] with n_rows x pmax
 // at most twice the item target (the grid; workgroups beyond a row's actual
-// segment count exit at once).  Rows are split only when the call has at most
-// 4 x CUs rows.
+// segment count exit at once), and at least 2 while the call has at most
+// 2 x CUs rows; above that no row is split.
 int32_t plan_pmax(int32_t n_rows, int cus) {
     const int64_t lim = 2ll * plan_items(cus);
     int32_t p = 1;
     while (p < kMaxSplit && (int64_t)(p * 2) * n_rows <= lim) p *= 2;
+    // while the call's rows fit the resident workgroups at once, long rows
+    // may still be halved (with more rows, halving cost the edge-case batch
+    // more in its rows' exact recoveries than it saved elsewhere)
+    if (p == 1 && (int64_t)n_rows <= 2ll * cus) p = 2;
     return p;
 }
 
