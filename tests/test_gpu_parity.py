@@ -470,3 +470,18 @@ def test_split_rows_with_an_overflowed_region(topk):
     gt, st = parity(topk, wl)
     say("routes", st)
     assert st["exact_overflow"] > 0 and st["primary"] + st["band"] > 0
+
+
+def test_many_rows_halves_the_long_ones(topk):
+    """A call of more rows than the item target but within the resident
+    workgroups (450 rows): rows longer than the mean are cut in two."""
+    rng = np.random.default_rng(41)
+    n = 450
+    lens = np.where(rng.random(n) < 0.2, rng.integers(60000, 131072, n),
+                    rng.integers(3000, 30000, n)).astype(np.int32)
+    rows = [W.decode_mixture_row(rng, int(L)).astype(np.float32) for L in lens]
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload("many rows", np.concatenate(rows), offs, lens, 2048, "")
+    gt, st = parity(topk, wl)
+    say("routes", st)
+    assert st["errors"] == 0
