@@ -171,6 +171,14 @@ int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream
 int topk_ragged_debug_coarse(const float *x, int64_t n, uint16_t *out_c, void *stream);
 int topk_ragged_debug_cutoffs(uint32_t *out_cut, void *stream);
 
+/* For tests of the split-row wait (Section 4.5 mapping): the number of polls a
+ * segment makes for segment 0's published boundaries before it builds the
+ * view itself (counted in topk_ragged_stats.wait_fallback), for the calls
+ * launched after it; 0 restores the default.  Results do not depend on it.
+ * Process-wide, not synchronised with concurrent calls.  Returns TOPK_OK, or
+ * TOPK_EINVAL for a negative count. */
+int topk_ragged_debug_set_spin_limit(int32_t polls);
+
 /* Human-readable text for a status code. */
 const char *topk_ragged_status_str(int status);
 

@@ -113,6 +113,7 @@ struct KArgs {
     int32_t q0, q1;
     int32_t l_samp_min;
     int32_t cap;
+    int32_t spin_limit; // polls of the boundary word before a segment builds the view itself
 #ifdef TOPK_PHASE_TIMERS
     uint64_t *timers; // 32 words per workgroup, see PHASE_MARK
 #endif
@@ -2021,7 +2022,7 @@ topk_ragged_kernel(KArgs a) {
             if (!have) {
                 if (tid == 0) {
                     uint32_t v = 0;
-                    for (int spin = 0; spin < kSpinLimit; spin++) {
+                    for (int spin = 0; spin < a.spin_limit; spin++) {
                         v = __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                         if (v & 0x80000000u) break;
                         __builtin_amdgcn_s_sleep(1);
@@ -2420,6 +2421,10 @@ topk_ragged_policy policy_for_k(int32_t K) {
     return p;
 }
 
+// Boundary-word polls before a segment builds the view itself; 0 = kSpinLimit
+// (tests lower it to exercise that path).
+int32_t g_spin_limit = 0;
+
 int32_t sample_rank(int32_t K, int32_t num, int32_t den, int32_t s_log2) {
     const int64_t d = (int64_t)den << s_log2;
     return (int32_t)(((int64_t)num * K + d - 1) / d);
@@ -2516,6 +2521,7 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     a.l_samp_min = pol.l_samp_min >= 0 ? pol.l_samp_min
                                        : (int32_t)(floor_k < 0x7FFFFFFF ? floor_k : 0x7FFFFFFF);
     a.cap = pol.cap;
+    a.spin_limit = g_spin_limit > 0 ? g_spin_limit : kSpinLimit;
     hipLaunchKernelGGL(topk_ragged_kernel, dim3((unsigned)(n_rows * pmax)), dim3(kBlock), 0,
                        (hipStream_t)stream, a);
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
@@ -2543,6 +2549,12 @@ int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream
     out->errors = st[kStatErrors];
     hipLaunchKernelGGL(stats_reset_kernel, dim3(1), dim3(64), 0, s, hdr);
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
+}
+
+int topk_ragged_debug_set_spin_limit(int32_t polls) {
+    if (polls < 0) return TOPK_EINVAL;
+    g_spin_limit = polls;
+    return TOPK_OK;
 }
 
 int topk_ragged_debug_coarse(const float *x, int64_t n, uint16_t *out_c, void *stream) {

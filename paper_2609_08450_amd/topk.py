@@ -100,6 +100,8 @@ def lib():
         L.topk_ragged_debug_coarse.restype = ctypes.c_int
         L.topk_ragged_debug_cutoffs.argtypes = [P, P]
         L.topk_ragged_debug_cutoffs.restype = ctypes.c_int
+        L.topk_ragged_debug_set_spin_limit.argtypes = [ctypes.c_int32]
+        L.topk_ragged_debug_set_spin_limit.restype = ctypes.c_int
         L.topk_ragged_status_str.argtypes = [ctypes.c_int]
         L.topk_ragged_status_str.restype = ctypes.c_char_p
         _lib = L
@@ -207,6 +209,12 @@ def debug_coarse(x, out_c, stream=None) -> None:
 def debug_cutoffs(out_cut, stream=None) -> None:
     _check(lib().topk_ragged_debug_cutoffs(_ptr(out_cut, torch.int32, "out_cut"),
                                            _stream(stream)), "topk_ragged_debug_cutoffs")
+
+
+def debug_set_spin_limit(polls: int) -> None:
+    """Polls of the boundary word before a split segment builds the view
+    itself, for later calls (0 = default); see include/topk_ragged.h."""
+    _check(lib().topk_ragged_debug_set_spin_limit(polls), "topk_ragged_debug_set_spin_limit")
 
 
 class TopK:

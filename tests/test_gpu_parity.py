@@ -485,3 +485,21 @@ def test_many_rows_halves_the_long_ones(topk):
     gt, st = parity(topk, wl)
     say("routes", st)
     assert st["errors"] == 0
+
+
+def test_segments_that_stop_waiting_build_the_view(topk):
+    """With one poll allowed, split segments that do not see segment 0's
+    boundaries at once build the whole view themselves (a small view, and a
+    shared large one): same boundaries, routes and selections."""
+    rng = np.random.default_rng(43)
+    lens = np.array([524288, 600000, 90000, 131072, 40000, 70000], np.int32)
+    rows = [W.decode_mixture_row(rng, int(L)).astype(np.float32) for L in lens]
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload("spin limit 1", np.concatenate(rows), offs, lens, 2048, "")
+    topk.debug_set_spin_limit(1)
+    try:
+        gt, st = parity(topk, wl)
+    finally:
+        topk.debug_set_spin_limit(0)
+    say("routes", st)
+    assert st["wait_fallback"] > 0
