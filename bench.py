@@ -341,13 +341,17 @@ def main():
                     help="kernel FETCH_SIZE, kernel WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE "
                          "counter CSVs from rocprofv3 --pmc; writes the traffic file and exits")
     ap.add_argument("--copy-mib", type=int, default=1024, help="size of the calibration copy")
+    ap.add_argument("--traffic-out", default=None,
+                    help="where --traffic-summary writes (default: the decode traffic file "
+                         "that the bench line reports)")
     ap.add_argument("--ablation", choices=ABLATIONS, default=None,
                     help="instead of the bench line, one JSON line per policy variant (the "
                          "paper's ablations on synthetic rows; --config picks the rows)")
     args = ap.parse_args()
 
     if args.traffic_summary:
-        traffic_summary(args.traffic_summary, args.config, args.copy_mib, TRAFFIC_FILE)
+        traffic_summary(args.traffic_summary, args.config, args.copy_mib,
+                        args.traffic_out or TRAFFIC_FILE)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
