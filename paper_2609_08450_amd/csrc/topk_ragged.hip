@@ -12,11 +12,13 @@
 //                     eq:method:primary-threshold) -> Phase 2 (complete-row
 //                     certify + compact, eq:method:candidate-set) -> band or
 //                     exact recovery when underfilled -> Phase 3 refinement.
-//   sampled, P segs   segment 0 runs Phase 1 and publishes the endpoints;
-//                     every segment certifies and compacts its contiguous
-//                     part of the row (eq:method:split-local); the last
-//                     segment to arrive merges the candidate ranges
-//                     (eq:method:split-reduce) and finishes the row.
+//   sampled, P segs   segment 0 runs Phase 1 and publishes the endpoints
+//                     (a large view is shared: each segment histograms its
+//                     own part, the last to add publishes); every segment
+//                     certifies and compacts its contiguous part of the row
+//                     (eq:method:split-local); the last segment to arrive
+//                     merges the candidate ranges (eq:method:split-reduce)
+//                     and finishes the row.
 //
 // Keys: asc = order-preserving uint32 of the FP32 bits; the descending key
 // kappa32 = ~asc (Section 4.3) is what the radix digits are taken from.  The
