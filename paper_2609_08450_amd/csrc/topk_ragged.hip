@@ -66,11 +66,19 @@ constexpr size_t kRowBlockBytes = kRowStateBytes + kViewHistBytes + 2 * kFront *
 constexpr int64_t kCoopView = 4096;
 // Most segments a row may have for its segments to publish per wave.
 constexpr int64_t kWavePublishMaxSegs = 16;
+// Calls whose rows each take one workgroup (more rows than can be resident)
+// run their rows longest first: a pre-pass writes the order, one 16-byte
+// entry (row, length, offset) per row, into a fixed region after the header,
+// for calls of up to kOrderMaxRows rows.
+constexpr int kOrderMaxRows = 16384;
+constexpr size_t kOrderBytes = (size_t)kOrderMaxRows * 16;
+constexpr int kOrderBlock = 1024;
+constexpr int kOrderPer = kOrderMaxRows / kOrderBlock;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 // Per-row state of a split row.  Row r of a split call owns the workspace
-// block at kHeaderBytes + r * kRowBlockBytes: this state, padded to 256
+// block at kHeaderBytes + kOrderBytes + r * kRowBlockBytes: this state, padded to 256
 // bytes, the 2048-bin view histogram that segments sharing the view add
 // into, then kFront candidates as 64-bit (index | FP32 bits << 32) words
 // (the segments' A(tau1) entries, concatenated).  Every field and entry is
@@ -107,6 +115,7 @@ struct KArgs {
     int32_t *trace;
     WsHeader *hdr;
     char *rows;     // per-row blocks of kRowBlockBytes
+    const uint4 *order; // rows longest first (row, length, offset), or NULL: item = row
     int32_t n_rows;
     int32_t K;
     int32_t pmax;
@@ -1899,17 +1908,26 @@ topk_ragged_kernel(KArgs a) {
     TimerFlush timer_flush{a.timers};
 #endif
     const int p = item / a.n_rows;
-    const int r = item - p * a.n_rows;
     // Every load the prologue needs goes out at once: the row's length and
-    // offset, the workspace header, and this thread's first term of the
+    // offset (from the longest-first order when the call has one, p = 0
+    // then), the workspace header, and this thread's first term of the
     // segment plan's length sum (used only when rows may be split).
-    const int32_t len_r = a.lens[r];
-    const int64_t off = a.offs[r];
+    // (all loaded unconditionally and selected afterwards: a branch here
+    // would cost a second round trip; with an order, p = 0 and item < n_rows)
+    const bool ordered = a.order != nullptr;
+    const int ri = item - p * a.n_rows;
+    const uint4 e = *(ordered ? a.order + item : reinterpret_cast<const uint4 *>(a.hdr));
+    const int32_t len_i = a.lens[ri];
+    const int64_t off_i = a.offs[ri];
     const int32_t len0_raw = a.lens[min(tid, a.n_rows - 1)];
     const uint4 hw = *reinterpret_cast<const uint4 *>(a.hdr); // magic, split_rows, max_rows
     // (keeps the compiler from sinking each load to its first use, which
-    // would make them four round trips instead of one)
-    asm volatile("" ::"s"(len_r), "s"(off), "s"(hw.x), "s"(hw.y), "s"(hw.z), "v"(len0_raw));
+    // would make them several round trips instead of one)
+    asm volatile("" ::"s"(e.x), "s"(e.y), "s"(e.z), "s"(e.w), "s"(len_i), "s"(off_i), "s"(hw.x),
+                 "s"(hw.y), "s"(hw.z), "v"(len0_raw));
+    const int r = ordered ? (int)e.x : ri;
+    const int32_t len_r = ordered ? (int32_t)e.y : len_i;
+    const int64_t off = ordered ? (int64_t)(((uint64_t)e.w << 32) | e.z) : off_i;
     const int64_t L = (int64_t)max(len_r, 0);
     const float *row = a.scores + off;
     PHASE_MARK(a, 0);
@@ -2284,6 +2302,69 @@ topk_ragged_kernel(KArgs a) {
     if (split && tid == 0) reset_row_state(rs);
 }
 
+// Length class of a row for the longest-first order: 8 classes per octave
+// of the length (rows shorter than 8 elements: the length itself), so the
+// class never decreases with the length; at most 247.
+__device__ __forceinline__ uint32_t length_class(int32_t L) {
+    if (L < 8) return L <= 0 ? 0u : (uint32_t)L;
+    const uint32_t e = 31u - (uint32_t)__clz(L);
+    return e * 8u + (((uint32_t)L >> (e - 3u)) & 7u);
+}
+
+// Pre-pass of a call whose rows each take one workgroup: a counting sort of
+// the rows by length class, longest first (any order within a class), into
+// order[0, n) as (row, length, offset low, offset high).  One workgroup;
+// n <= kOrderMaxRows.  Thread t takes rows [kOrderPer t, kOrderPer (t + 1)),
+// and a run of equal classes among them takes one LDS atomic: rows of
+// similar length would otherwise all add into one counter at once.
+__global__ __launch_bounds__(kOrderBlock) void row_order_kernel(const int64_t *offs,
+                                                                const int32_t *lens, int32_t n,
+                                                                uint4 *order) {
+    constexpr uint32_t kNone = 256; // class of a position past the last row
+    __shared__ uint32_t cnt[256];
+    const int tid = threadIdx.x;
+    const int i0 = tid * kOrderPer;
+    if (tid < 256) cnt[tid] = 0;
+    int32_t Ls[kOrderPer];
+    int64_t Os[kOrderPer]; // loaded with the lengths: one round trip to memory
+#pragma unroll
+    for (int j = 0; j < kOrderPer; j++) {
+        Ls[j] = i0 + j < n ? lens[i0 + j] : 0;
+        Os[j] = i0 + j < n ? offs[i0 + j] : 0;
+    }
+    uint32_t cls[kOrderPer], run[kOrderPer]; // run[j]: rows of j's run from j on
+#pragma unroll
+    for (int j = 0; j < kOrderPer; j++) cls[j] = i0 + j < n ? length_class(Ls[j]) : kNone;
+    run[kOrderPer - 1] = 1;
+#pragma unroll
+    for (int j = kOrderPer - 2; j >= 0; j--) run[j] = cls[j] == cls[j + 1] ? run[j + 1] + 1 : 1;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kOrderPer; j++)
+        if (cls[j] != kNone && (j == 0 || cls[j] != cls[j - 1])) atomicAdd(&cnt[cls[j]], run[j]);
+    __syncthreads();
+    if (tid < 64) {
+        // start of class c = rows in classes above c; lane l holds classes
+        // 255 - 4l .. 252 - 4l, longest first
+        uint32_t c4[4], t = 0;
+#pragma unroll
+        for (int k = 0; k < 4; k++) { c4[k] = cnt[255 - 4 * tid - k]; t += c4[k]; }
+        uint32_t acc = wave_incl_scan(t) - t;
+#pragma unroll
+        for (int k = 0; k < 4; k++) { cnt[255 - 4 * tid - k] = acc; acc += c4[k]; }
+    }
+    __syncthreads();
+    uint32_t pos = 0;
+#pragma unroll
+    for (int j = 0; j < kOrderPer; j++) {
+        if (cls[j] == kNone) continue;
+        if (j == 0 || cls[j] != cls[j - 1]) pos = atomicAdd(&cnt[cls[j]], run[j]);
+        else pos++;
+        const uint64_t o = (uint64_t)Os[j];
+        order[pos] = make_uint4((uint32_t)(i0 + j), (uint32_t)Ls[j], (uint32_t)o, (uint32_t)(o >> 32));
+    }
+}
+
 // Workspace set-up: header and zeroed per-row state (the candidate arrays
 // need no initialisation: only entries below the published count are read).
 __global__ void ws_init_kernel(WsHeader *hdr, char *rows, uint32_t split_rows, uint32_t max_rows,
@@ -2371,7 +2452,7 @@ int32_t plan_pmax(int32_t n_rows, int cus) {
 }
 
 size_t ws_bytes(uint32_t split_rows) {
-    return kHeaderBytes + (size_t)split_rows * kRowBlockBytes;
+    return kHeaderBytes + kOrderBytes + (size_t)split_rows * kRowBlockBytes;
 }
 
 topk_ragged_policy default_policy() {
@@ -2465,7 +2546,7 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
     const uint32_t sr = split_rows_for(max_rows, di.cus);
     if (bytes < ws_bytes(sr)) return TOPK_EWORKSPACE;
     WsHeader *hdr = static_cast<WsHeader *>(workspace);
-    char *rows = static_cast<char *>(workspace) + kHeaderBytes;
+    char *rows = static_cast<char *>(workspace) + kHeaderBytes + kOrderBytes;
     const int blocks = sr ? (int)(sr < 1024 ? sr : 1024) : 1;
     hipLaunchKernelGGL(ws_init_kernel, dim3(blocks), dim3(64), 0, (hipStream_t)stream, hdr, rows,
                        sr, (uint32_t)max_rows, (uint32_t)kCap);
@@ -2507,7 +2588,8 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     a.out_val = out_val;
     a.trace = row_trace;
     a.hdr = static_cast<WsHeader *>(workspace);
-    a.rows = static_cast<char *>(workspace) + kHeaderBytes;
+    a.rows = static_cast<char *>(workspace) + kHeaderBytes + kOrderBytes;
+    a.order = nullptr;
     a.n_rows = n_rows;
     a.K = K;
     a.pmax = pmax;
@@ -2524,6 +2606,15 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
                                        : (int32_t)(floor_k < 0x7FFFFFFF ? floor_k : 0x7FFFFFFF);
     a.cap = pol.cap;
     a.spin_limit = g_spin_limit > 0 ? g_spin_limit : kSpinLimit;
+    if (pmax == 1 && n_rows <= kOrderMaxRows) {
+        // more rows than resident workgroups: longest rows first, so that
+        // the last to start is short
+        uint4 *order = reinterpret_cast<uint4 *>(static_cast<char *>(workspace) + kHeaderBytes);
+        hipLaunchKernelGGL(row_order_kernel, dim3(1), dim3(kOrderBlock), 0, (hipStream_t)stream,
+                           row_offsets, row_lengths, n_rows, order);
+        if (hipGetLastError() != hipSuccess) return TOPK_ELAUNCH;
+        a.order = order;
+    }
     hipLaunchKernelGGL(topk_ragged_kernel, dim3((unsigned)(n_rows * pmax)), dim3(kBlock), 0,
                        (hipStream_t)stream, a);
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;

@@ -487,6 +487,30 @@ def test_many_rows_halves_the_long_ones(topk):
     assert st["errors"] == 0
 
 
+@pytest.mark.parametrize("n", [1500, 16385])
+def test_many_rows_run_longest_first(topk, n):
+    """Calls whose rows each take one workgroup run them longest first
+    (1500 rows, lengths from empty to 200K in random order, stored in the
+    buffer in another order than their indices); above the order's row limit
+    (16385 short rows) they run in index order.  Same selections either way."""
+    rng = np.random.default_rng(47 + n)
+    if n <= 2000:
+        lens = np.where(rng.random(n) < 0.15, rng.integers(100000, 200000, n),
+                        rng.integers(0, 12000, n)).astype(np.int32)
+        lens[rng.choice(n, 20, replace=False)] = 0
+    else:
+        lens = rng.integers(1, 4000, n).astype(np.int32)
+    rows = [W.decode_mixture_row(rng, int(L)).astype(np.float32) for L in lens]
+    place = rng.permutation(n)             # row place[j] is the j-th in the buffer
+    offs = np.zeros(n, np.int64)
+    offs[place] = np.concatenate([[0], np.cumsum(lens[place][:-1])])
+    buf = np.concatenate([rows[r] for r in place])
+    wl = W.Workload("longest first", buf, offs, lens, 2048, "")
+    gt, st = parity(topk, wl)
+    say("routes", st)
+    assert st["errors"] == 0
+
+
 def test_segments_that_stop_waiting_build_the_view(topk):
     """With one poll allowed, split segments that do not see segment 0's
     boundaries at once build the whole view themselves (a small view, and a
