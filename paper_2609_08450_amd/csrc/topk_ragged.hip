@@ -2327,10 +2327,29 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(const int64_t *o
     if (tid < 256) cnt[tid] = 0;
     int32_t Ls[kOrderPer];
     int64_t Os[kOrderPer]; // loaded with the lengths: one round trip to memory
+    // (16-byte loads where the arrays allow: each thread's rows are
+    // contiguous, so the lanes of one load are 64 bytes apart)
+    const bool vec = ((reinterpret_cast<uintptr_t>(lens) | reinterpret_cast<uintptr_t>(offs)) &
+                      15u) == 0 && i0 + kOrderPer <= n;
+    if (vec) {
+        const int4 *l4 = reinterpret_cast<const int4 *>(lens + i0);
+        const longlong2 *o2 = reinterpret_cast<const longlong2 *>(offs + i0);
 #pragma unroll
-    for (int j = 0; j < kOrderPer; j++) {
-        Ls[j] = i0 + j < n ? lens[i0 + j] : 0;
-        Os[j] = i0 + j < n ? offs[i0 + j] : 0;
+        for (int q = 0; q < kOrderPer / 4; q++) {
+            const int4 v = l4[q];
+            Ls[4 * q] = v.x; Ls[4 * q + 1] = v.y; Ls[4 * q + 2] = v.z; Ls[4 * q + 3] = v.w;
+        }
+#pragma unroll
+        for (int q = 0; q < kOrderPer / 2; q++) {
+            const longlong2 v = o2[q];
+            Os[2 * q] = v.x; Os[2 * q + 1] = v.y;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kOrderPer; j++) {
+            Ls[j] = i0 + j < n ? lens[i0 + j] : 0;
+            Os[j] = i0 + j < n ? offs[i0 + j] : 0;
+        }
     }
     uint32_t cls[kOrderPer], run[kOrderPer]; // run[j]: rows of j's run from j on
 #pragma unroll
