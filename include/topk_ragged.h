@@ -142,9 +142,12 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
  *                by topk_ragged_workspace_init with max_rows >= n_rows; not
  *                shared by concurrent calls.
  * Row lengths and offsets stay on the device; the launch geometry depends
- * only on (n_rows, K, device).  If the workspace is invalid for n_rows the
+ * only on (n_rows, K, device).  A call of more than 2 x CUs and at most
+ * 16384 rows enqueues a one-workgroup pre-pass before the main kernel: it
+ * writes the order of the rows, longest first, into the workspace.  If the workspace is invalid for n_rows the
  * kernel writes -1 / -inf to every output and counts an error in the stats.
- * Returns TOPK_OK or an error code; nothing is enqueued on error. */
+ * Returns TOPK_OK or an error code; nothing is enqueued on an argument
+ * error. */
 int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
                 int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                 void *stream);

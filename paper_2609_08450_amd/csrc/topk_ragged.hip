@@ -2,7 +2,10 @@
 //
 // One kernel launch per call.  Work item = (row r, segment p); blockIdx.x =
 // p * n_rows + r, so every row's first segment is dispatched before any
-// second segment.  Each item is one 512-thread workgroup.
+// second segment.  Each item is one 512-thread workgroup.  A call whose rows
+// each take one workgroup and outnumber the resident workgroups (at most
+// 16384 rows) first runs a one-workgroup pre-pass that orders the rows
+// longest first; blockIdx.x then indexes that order.
 //
 //   L <= K            segment 0 writes the direct layout (Section 2.1).
 //   not sampled       segment 0 runs exact coarse recovery alone
