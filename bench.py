@@ -6,7 +6,10 @@ rotate over enough distinct copies of the batch (>= 512 MB in total) that the
 256 MB last-level cache cannot serve repeats; they are captured in HIP graphs
 (one call per graph node, as a serving loop would replay them) and replayed
 back-to-back on one stream.  HIP events on that stream bracket exactly
-`--steps` calls after `--warmup` untimed ones.
+`--steps` calls after exactly `--warmup` untimed ones; a busy kernel queued
+just before the first event keeps the host's graph launch out of the timed
+region.  `--rounds` more rounds of about 100 calls are timed separately and
+their median is reported beside the main figure.
 
 Metric: effective score-read bandwidth = 4 B x sum(L) per call / time per
 call, the algorithmic bytes of an exact selector (one complete read of every
@@ -59,9 +62,25 @@ def make_workload(config: int):
     return W.make(config)
 
 
-def cpu_baseline(wl, budget_s: float, threads: int):
-    """The oracle as it stands, on the host cores, over whole copies of the
-    batch until about budget_s seconds have passed."""
+def host_cpu():
+    """CPU model and the cores this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    return model, avail
+
+
+def _time_oracle(wl, budget_s: float, threads: int):
     import oracle
 
     oracle.topk_ragged(wl.scores[:0], wl.row_offsets[:0], wl.row_lengths[:0], wl.K, threads)
@@ -72,11 +91,31 @@ def cpu_baseline(wl, budget_s: float, threads: int):
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
+    return reps, el
+
+
+def cpu_baseline(wl, budget_s: float):
+    """The oracle as it stands, on the host cores: whole copies of the batch
+    until about budget_s seconds have passed with every available core (the
+    OpenMP thread count is capped by OMP_NUM_THREADS when that is set), and a
+    third of that with one thread."""
+    model, avail = host_cpu()
+    threads = avail
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        threads = min(threads, int(env))
+    reps, el = _time_oracle(wl, budget_s, threads)
+    reps1, el1 = _time_oracle(wl, budget_s / 3.0, 1)
     gbs = 4.0 * wl.total_len * reps / el / 1e9
+    gbs1 = 4.0 * wl.total_len * reps1 / el1 / 1e9
     return {"value": round(gbs, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} full batches ({wl.n_rows} rows, {wl.total_len} scores each) "
-                      f"in {el:.1f} s, {threads} OpenMP threads, plain sort oracle",
-            "us_per_call": round(el / reps * 1e6, 1)}
+                      f"in {el:.1f} s on {threads} OpenMP threads; plain sort oracle",
+            "us_per_call": round(el / reps * 1e6, 1),
+            "single_thread": {"value": round(gbs1, 3), "unit": "GB/s",
+                              "us_per_call": round(el1 / reps1 * 1e6, 1),
+                              "sample": f"{reps1} full batches in {el1:.1f} s"},
+            "cpu_model": model, "cpus_available": avail}
 
 
 def copy_calibration(mib: int, steps: int, warmup: int):
@@ -152,11 +191,42 @@ def traffic_summary(paths, config: int, copy_mib: int, out_path: str):
     print(json.dumps(out))
 
 
-def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0):
-    """Times `steps` topk_ragged calls on workload wl (policy None = default)
-    over rotated device copies, captured in graphs and replayed on one stream
-    between HIP events.  Returns (ms per call, route counts of one call,
-    copies, calls per graph, warm-up calls)."""
+SPACER_CYCLES = 20_000_000  # ~10 ms busy kernel ahead of a timed region
+
+
+def upload_graph(g, stream) -> bool:
+    """hipGraphUpload of a captured graph's executable on `stream`: the
+    runtime's one-time copy of the graph to the device happens here rather
+    than inside the first timed replay.  Runs no kernel."""
+    import ctypes
+
+    try:
+        path = None
+        with open("/proc/self/maps") as fh:
+            for ln in fh:
+                if "libamdhip64" in ln:
+                    path = ln.split()[-1]
+                    break
+        hip = ctypes.CDLL(path or "libamdhip64.so")
+        hip.hipGraphUpload.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        hip.hipGraphUpload.restype = ctypes.c_int
+        rc = hip.hipGraphUpload(ctypes.c_void_p(g.raw_cuda_graph_exec()),
+                                ctypes.c_void_p(stream.cuda_stream))
+        stream.synchronize()
+        return rc == 0
+    except Exception:
+        return False
+
+
+def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0, rounds=0,
+               round_calls=100):
+    """Times exactly `steps` topk_ragged calls on workload wl (policy None =
+    the production call) over rotated device copies, captured in HIP graphs
+    and replayed on one stream between HIP events on that stream, after
+    exactly `warmup` untimed calls.  A busy kernel is queued ahead of the
+    first event so that the host's graph launch is not inside the timed
+    region.  With rounds > 0, also times that many separate rounds of about
+    round_calls calls each and reports their median.  Returns a dict."""
     import torch
 
     from paper_2609_08450_amd import topk
@@ -185,26 +255,41 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0):
             topk.topk_ragged_ex(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws,
                                 policy, None, s)
 
-    # one graph with G consecutive calls over rotating copies; a tail graph for
-    # the remainder, so exactly `steps` calls are timed
+    # a graph of G consecutive calls over rotating copies, and a tail graph
+    # for the remainder, so that exactly `steps` calls are timed
     G = calls_per_graph or copies
     G = max(1, min(G, steps)) if steps > 0 else 1
 
-    def capture(ncalls, first):
+    def capture(ncalls):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
             for j in range(ncalls):
-                call(first + j, torch.cuda.current_stream())
+                call(j, torch.cuda.current_stream())
         return g
 
+    # warm-up: exactly `warmup` untimed calls (eager; the first loads the code)
     with torch.cuda.stream(stream):
-        for i in range(min(warmup, 3)):
-            call(i, stream)           # eager warm-up (code object load)
+        for i in range(warmup):
+            call(i, stream)
     stream.synchronize()
-    g_main = capture(G, 0)
+    g_main = capture(G)
     rem = steps % G
-    g_tail = capture(rem, 0) if rem else None
+    g_tail = capture(rem) if rem else None
     stream.synchronize()
+    uploaded = upload_graph(g_main, stream) and (g_tail is None or upload_graph(g_tail, stream))
+
+    def timed(fn):
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(SPACER_CYCLES)
+            ev0.record(stream)
+            fn()
+            ev1.record(stream)
+        ev1.synchronize()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1)
 
     def run(nsteps):
         reps, tail = divmod(nsteps, G)
@@ -214,31 +299,26 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0):
             assert tail == rem
             g_tail.replay()
 
-    # warmup: whole graph replays plus the tail, untimed
-    wreps = max(1, warmup // G)
-    for _ in range(wreps):
-        g_main.replay()
-    torch.cuda.synchronize()
+    ms = timed(lambda: run(steps))
+    out = {"ms_per_call": ms / steps, "copies": copies, "copies_touched": min(copies, steps),
+           "calls_per_graph": G, "warmup_calls": warmup, "graphs_uploaded": uploaded}
 
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        ev0.record(stream)
-        run(steps)
-        ev1.record(stream)
-    ev1.synchronize()
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1)
+    if rounds > 0:
+        reps = max(1, -(-round_calls // G))
+        per = sorted(timed(lambda: [g_main.replay() for _ in range(reps)]) / (reps * G)
+                     for _ in range(rounds))
+        out["rounds"] = {"rounds": rounds, "calls_per_round": reps * G,
+                         "ms_per_call_median": per[len(per) // 2],
+                         "ms_per_call_min": per[0], "ms_per_call_max": per[-1]}
 
     # outside the timed region: route counts of one call
     topk.read_stats(ws, stream)
     with torch.cuda.stream(stream):
         call(0, stream)
-    routes = topk.read_stats(ws, stream)
+    out["routes"] = topk.read_stats(ws, stream)
     del bufs, g_main, g_tail
     torch.cuda.synchronize()
-    return ms / steps, routes, copies, G, wreps * G
+    return out
 
 
 ABLATIONS = ("margin", "stride", "rescue", "crossover", "k", "recal", "recal-crossover", "batch")
@@ -316,7 +396,8 @@ def ablation(name, wl, steps, warmup):
                 variants.append((f"K={K} L={L} sampled", wlL, pol(**dict(kp, l_samp_min=0))))
                 variants.append((f"K={K} L={L} exact", wlL, pol(l_samp_min=0x7FFFFFFF)))
     for label, w, p in variants:
-        ms, routes, copies, _, _ = time_calls(w, p, steps, warmup)
+        t = time_calls(w, p, steps, warmup)
+        ms, routes = t["ms_per_call"], t["routes"]
         print(json.dumps({"ablation": name, "variant": label, "rows": w.n_rows, "K": w.K,
                           "us_per_call": round(ms * 1e3, 3),
                           "gbs": round(4.0 * w.total_len / (ms * 1e-3) / 1e9, 2),
@@ -333,8 +414,13 @@ def main():
     ap.add_argument("--config", type=int, default=2,
                     help="workload: 1 tiny, 2 decode (headline), 3 chunked prefill, 4 long split, 5 edge mix")
     ap.add_argument("--calls-per-graph", type=int, default=0, help="0 = number of rotated copies")
+    ap.add_argument("--rounds", type=int, default=7,
+                    help="after the timed steps, this many separately timed rounds of about 100 "
+                         "calls (median reported); 0 = none")
     ap.add_argument("--no-rotate", action="store_true", help="reuse one copy (cache-resident input)")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time; 0 = skip")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of all-core oracle time (plus a third of it on one thread); "
+                         "0 = skip")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only time a plain device copy of MIB MiB (counter calibration)")
     ap.add_argument("--traffic-summary", nargs=4, metavar="CSV",
@@ -369,8 +455,9 @@ def main():
     if args.ablation:
         ablation(args.ablation, wl, args.steps, args.warmup)
         return
-    ms_per_step, routes, copies, G, wreps = time_calls(wl, None, args.steps, args.warmup,
-                                                       not args.no_rotate, args.calls_per_graph)
+    t = time_calls(wl, None, args.steps, args.warmup, not args.no_rotate, args.calls_per_graph,
+                   rounds=args.rounds)
+    ms_per_step = t["ms_per_call"]
     K, n = wl.K, wl.n_rows
     batch_bytes = 4 * wl.scores.size
     alg_bytes = 4.0 * wl.total_len
@@ -383,7 +470,7 @@ def main():
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": wreps,
+        "warmup": t["warmup_calls"],
         "ms_per_step": round(ms_per_step, 6),
         "us_per_call": round(ms_per_step * 1e3, 3),
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
@@ -394,18 +481,25 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name + ": " + wl.description, "rows": n, "K": K,
                    "sum_len": wl.total_len, "bytes_per_call": int(alg_bytes),
-                   "rotated_copies": copies, "calls_per_graph": G,
-                   "rotated_bytes": copies * batch_bytes},
+                   "copies_touched": t["copies_touched"], "calls_per_graph": t["calls_per_graph"],
+                   "touched_bytes": t["copies_touched"] * batch_bytes,
+                   "graphs_uploaded": t["graphs_uploaded"]},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
-        "routes": routes,
+        "routes": t["routes"],
         "kernel": "topk_ragged_kernel",
         "kernel_source_sha256_16": kernel_source_hash(),
     }
+    if "rounds" in t:
+        rd = t["rounds"]
+        result["rounds"] = {"rounds": rd["rounds"], "calls_per_round": rd["calls_per_round"],
+                            "us_per_call_median": round(rd["ms_per_call_median"] * 1e3, 3),
+                            "us_per_call_min": round(rd["ms_per_call_min"] * 1e3, 3),
+                            "us_per_call_max": round(rd["ms_per_call_max"] * 1e3, 3),
+                            "gbs_median": round(alg_bytes / (rd["ms_per_call_median"] * 1e-3) / 1e9, 2)}
     if args.cpu_budget > 0:
-        threads = min(16, os.cpu_count() or 1)
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget, threads)
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)

@@ -56,6 +56,9 @@ extern "C" {
  * (topk_ragged_policy_for_k) sends every row of a larger K to the exact
  * route. */
 #define TOPK_K_MAX 16384
+/* Longest row, in elements: the kernels address a row's 16-byte vectors with
+ * 32-bit byte offsets from its base. */
+#define TOPK_L_MAX 0x3FFFFFFB
 /* Frontier capacity of one workgroup, in (index, key) pairs. */
 #define TOPK_FRONTIER_CAP 6144
 /* Words per row written by topk_ragged_ex when row_trace is not NULL. */
@@ -85,13 +88,19 @@ typedef struct topk_ragged_policy {
     int32_t cap;        /* frontier capacity, 1 <= cap <= TOPK_FRONTIER_CAP */
 } topk_ragged_policy;
 
-/* Route counters accumulated in the workspace (one increment per row with
- * L > K or L <= K), and error/diagnostic counts. */
+/* Route counters accumulated in the workspace (one increment per row), and
+ * error/diagnostic counts.  The routes are the outcomes of certification
+ * (Section 4.3: primary proposal, band of eq:method:rescue-band, exact coarse
+ * recovery of eq:method:exact-init); their fractions over the rows of a call
+ * are the primary-underfill and residual exact-recovery rates that the
+ * paper's ablations report (Section 6.4, "Retention margin" and "Conditional
+ * rescue"). */
 typedef struct topk_ragged_stats {
     uint64_t route[6];     /* indexed by TOPK_ROUTE_* (flag stripped) */
     uint64_t reread;       /* rows that took the re-read fallback */
     uint64_t wait_fallback;/* split segments that recomputed the view locally */
-    uint64_t errors;       /* calls rejected on the device (bad workspace) */
+    uint64_t errors;       /* rejected on the device: one per call with a bad
+                              workspace, one per row longer than TOPK_L_MAX */
 } topk_ragged_stats;
 
 /* Fills *out with the evaluated configuration above (the policy for K
@@ -113,17 +122,28 @@ int topk_ragged_default_policy(topk_ragged_policy *out);
 int topk_ragged_policy_for_k(int32_t K, topk_ragged_policy *out);
 
 /* Bytes of workspace needed for calls with n_rows <= max_rows and this K on
- * the current device.  Independent of row lengths: per-row state is kept only
- * for rows split across workgroups, and at most 4 x (compute units) rows are
- * ever split.  Returns 0 for invalid arguments. */
+ * the current device.  The serving path needs a workspace bounded
+ * independently of the batch's contents (Section 2.1, "Deployment
+ * requirements"), and the plan that sizes it is fixed before capture from the
+ * row capacity and the device (Section 5.5, "Shape-stable dispatch"): the
+ * size depends only on (max_rows, K, device), never on row lengths.  Per-row
+ * state is kept only for rows split across workgroups, and at most
+ * 4 x (compute units) rows are ever split.  Pure host computation; returns 0
+ * for invalid arguments (max_rows < 0, K outside [1, TOPK_K_MAX]). */
 size_t topk_ragged_workspace_size(int32_t max_rows, int32_t K);
 
 /* One-time initialisation of a workspace of `bytes` bytes (enqueued on
- * `stream` with kernels only, no memset nodes).  The workspace must be
- * 256-byte aligned, as hipMalloc returns (this call, topk_ragged and
- * topk_ragged_read_stats return TOPK_EINVAL otherwise).  Must run before the
- * first topk_ragged call on that workspace.  Kernels leave the workspace ready for
- * the next call, so graph replays need no re-initialisation. */
+ * `stream` with kernels only, no memset nodes): writes the header (tag,
+ * capacities) and zeroes every counter and per-row state.  The paper's
+ * dispatch restores its persistent counters on the device so that replays
+ * need no host work (Section 5.5, "Shape-stable dispatch"); here every call's
+ * kernels return the state they used to zero, so this runs once, before the
+ * first topk_ragged call on that workspace, and graph replays need no
+ * re-initialisation.  workspace: device memory owned by the caller, 256-byte
+ * aligned (as hipMalloc returns), at least topk_ragged_workspace_size(max_rows,
+ * K) bytes.  Returns TOPK_EINVAL for a null or misaligned workspace or
+ * invalid max_rows / K, TOPK_EWORKSPACE for a size below that, TOPK_ELAUNCH if
+ * the launch fails. */
 int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, int32_t K,
                                void *stream);
 
@@ -133,7 +153,9 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
  *                back-to-back or padded to a pitch (row_offsets[r] = r*pitch);
  *                any 4-byte alignment is accepted.  Must be free of NaN.
  *   row_offsets  device, int64 [n_rows], element offsets (>= 0).
- *   row_lengths  device, int32 [n_rows], valid lengths (negative = 0).
+ *   row_lengths  device, int32 [n_rows], valid lengths (negative = 0), at
+ *                most TOPK_L_MAX; a longer row is not selected: its outputs
+ *                are -1 / -inf and the stats count an error.
  *   n_rows       >= 0; 0 is a no-op.
  *   K            1 <= K <= TOPK_K_MAX.
  *   out_idx      device, int32 [n_rows x K], row-relative indices.
@@ -153,18 +175,30 @@ int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *
                 void *stream);
 
 /* topk_ragged with an explicit policy (NULL = topk_ragged_policy_for_k(K),
- * which is also what topk_ragged uses) and an optional
- * per-row trace (device, int32 [n_rows x TOPK_TRACE_WORDS], NULL = none):
- *   [0] route (TOPK_ROUTE_*, TOPK_ROUTE_REREAD_FLAG or-ed in), [1] view size
- *   |V| (-1 if L <= K), [2] tau0, [3] tau1 (-1 if not sampled), [4] C(tau0),
- *   [5] C(tau1) (-1 if not evaluated), [6] tau_star (-1 unless exact coarse
- *   recovery ran), [7] |Q0| entering refinement (-1 if L <= K). */
+ * which is also what topk_ragged uses) and an optional per-row trace (device,
+ * int32 [n_rows x TOPK_TRACE_WORDS], caller-owned, NULL = none) of the
+ * integers that decide the row's route, in the paper's notation:
+ *   [0] route (TOPK_ROUTE_*, TOPK_ROUTE_REREAD_FLAG or-ed in);
+ *   [1] view size |V| (eq:method:view; -1 if L <= K);
+ *   [2] tau0, [3] tau1: the primary and nested coarse boundaries of
+ *       eq:method:primary-threshold (-1 if not sampled);
+ *   [4] C(tau0): the admitted count of eq:method:candidate-set (Section 4.3);
+ *   [5] C(tau1), evaluated only when C(tau0) < K (the band of
+ *       eq:method:rescue-band; -1 otherwise);
+ *   [6] tau_star: the exact coarse boundary of eq:method:exact-init (-1
+ *       unless exact coarse recovery ran);
+ *   [7] |Q0|: the frontier entering refinement (Section 4.4; -1 if L <= K).
+ * Same errors as topk_ragged, plus TOPK_EINVAL for a policy out of range. */
 int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
                    int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                    const topk_ragged_policy *policy, int32_t *row_trace, void *stream);
 
-/* Copies the workspace's accumulated counters to *out (host) and resets them.
- * Synchronises `stream`.  For diagnostics outside timed regions. */
+/* Copies the workspace's accumulated route counters (see topk_ragged_stats:
+ * the per-route row counts behind the recovery rates of Section 6.4) to *out
+ * (host memory owned by the caller) and resets them.  Synchronises `stream`:
+ * for diagnostics outside timed or captured regions.  Returns TOPK_EINVAL for
+ * a null or misaligned workspace or a null out, TOPK_ELAUNCH if a HIP call
+ * fails. */
 int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream);
 
 /* Building-block probes for tests (device pointers):

@@ -1946,6 +1946,15 @@ topk_ragged_kernel(KArgs a) {
         }
         return;
     }
+    // A row longer than TOPK_L_MAX would overflow the 32-bit byte offsets of
+    // its vectors: it is not selected, and counted as an error.
+    if (L > (int64_t)TOPK_L_MAX) {
+        if (p == 0) {
+            write_error_row(a, r);
+            if (tid == 0) atomicAdd(&a.hdr->stats[kStatErrors], 1u);
+        }
+        return;
+    }
 
     if (L <= a.K) {
         if (p == 0) {

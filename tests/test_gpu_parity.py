@@ -88,9 +88,13 @@ def test_coarse_map_matches_oracle(topk):
 # ---------------------------------------------------------- workloads ----
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5])
-def test_parity_config(topk, cfg):
+@pytest.mark.parametrize("per_k", [False, True], ids=["evaluated", "per-K"])
+def test_parity_config(topk, cfg, per_k):
+    """Every row of the config, selections and route traces.  per-K is the
+    production call (no policy: topk_ragged_policy_for_k), which at K = 256
+    routes config 1's rows differently from the evaluated constants."""
     wl = W.make(cfg)
-    gt, st = parity(topk, wl, where=f"config {cfg} ({wl.name})")
+    gt, st = parity(topk, wl, where=f"config {cfg} ({wl.name})", per_k=per_k)
     say("routes", st)
 
 
@@ -100,9 +104,10 @@ def test_parity_adversarial_recovery(topk):
     assert st["exact_underfill"] > 0 and st["band"] + st["exact_underfill"] > 0
 
 
-def test_parity_chunked_prefill_sampled_rows(topk):
-    """Full 4096 x 131072 causal block on the GPU; 64 rows checked against the
-    oracle (first, last and seeded random rows), with traces."""
+def test_parity_chunked_prefill_all_rows(topk):
+    """The full 4096 x 131072 causal block on the GPU, called as production
+    calls it (no policy); every row's selection and route trace against the
+    oracle (its OpenMP threads over the rows of the host copy)."""
     import torch
 
     say("chunked prefill 4096 rows (device-built scores)")
@@ -110,18 +115,17 @@ def test_parity_chunked_prefill_sampled_rows(topk):
     n, K = lens.size, 2048
     o = torch.from_numpy(offs).cuda()
     l = torch.from_numpy(lens).cuda()
-    gi, gv, gt, st = run_hip(s, o, l, K, topk.default_policy(), True)
-    rng = np.random.default_rng(7)
-    rows = np.unique(np.concatenate([np.arange(8), np.arange(n - 8, n), rng.choice(n, 48, replace=False)]))
-    host = s.view(n, -1).cpu().numpy()
-    sub = W.Workload("prefill[rows]", np.concatenate([host[r, :lens[r]] for r in rows]),
-                     np.concatenate([[0], np.cumsum(lens[rows][:-1])]).astype(np.int64),
-                     lens[rows].astype(np.int32), K, "")
-    oi, ov = oracle.topk_ragged(sub.scores, sub.row_offsets, sub.row_lengths, K)
-    assert_same_selection(gi[rows], gv[rows], oi, ov, rows=rows, where="chunked prefill")
-    _, _, mt = oracle.route_model(sub.scores, sub.row_offsets, sub.row_lengths, K,
-                                  oracle_policy_of(topk.default_policy(), K), row_ids=rows)
-    assert np.array_equal(gt[rows], mt)
+    gi, gv, gt, st = run_hip(s, o, l, K, None, True)
+    host = s.reshape(-1).cpu().numpy()
+    del s
+    torch.cuda.synchronize()
+    say("oracle over all rows")
+    oi, ov = oracle.topk_ragged(host, offs, lens, K)
+    assert_same_selection(gi, gv, oi, ov, where="chunked prefill")
+    _, _, mt = oracle.route_model(host, offs, lens, K, oracle_policy_of(topk.policy_for_k(K), K))
+    bad = np.nonzero(np.any(gt != mt, axis=1))[0]
+    assert bad.size == 0, (f"chunked prefill: trace differs on {bad.size} rows, first row {bad[0]}: "
+                           f"gpu {gt[bad[0]].tolist()} oracle {mt[bad[0]].tolist()}")
     assert st["errors"] == 0 and st["direct"] == 0
     say("routes", st)
 
@@ -314,25 +318,30 @@ def test_repeated_calls_are_stable(topk):
 
 
 def test_graph_capture_and_replay(topk):
-    """Three calls (two workloads) captured in one HIP graph, replayed with host
-    work and synchronisation between replays; every replay must match the
-    eager results."""
+    """Four calls (three workloads, one of them with the order pre-pass)
+    captured in one HIP graph, replayed with host work and synchronisation
+    between replays; every replay must match the eager results."""
     import torch
 
-    wa, wb = W.decode(), W.adversarial(n_rows=128)
+    wa, wb, wc = W.decode(), W.adversarial(n_rows=128), W.adversarial(n_rows=1024)
     say("graph replay")
     sa, oa, la = device_arrays(wa)
     sb, ob, lb = device_arrays(wb)
+    sc, oc, lc = device_arrays(wc)
     K = 2048
     wsa = topk.alloc_workspace(wa.n_rows, K)
     wsb = topk.alloc_workspace(wb.n_rows, K)
-    outs = [(torch.empty((wa.n_rows, K), dtype=torch.int32, device="cuda"),
-             torch.empty((wa.n_rows, K), dtype=torch.float32, device="cuda")),
-            (torch.empty((wb.n_rows, K), dtype=torch.int32, device="cuda"),
-             torch.empty((wb.n_rows, K), dtype=torch.float32, device="cuda")),
-            (torch.empty((wa.n_rows, K), dtype=torch.int32, device="cuda"),
-             torch.empty((wa.n_rows, K), dtype=torch.float32, device="cuda"))]
-    calls = [(sa, oa, la, wa.n_rows, wsa), (sb, ob, lb, wb.n_rows, wsb), (sa, oa, la, wa.n_rows, wsa)]
+    wsc = topk.alloc_workspace(wc.n_rows, K)
+
+    def outs_for(w):
+        return (torch.empty((w.n_rows, K), dtype=torch.int32, device="cuda"),
+                torch.empty((w.n_rows, K), dtype=torch.float32, device="cuda"))
+
+    outs = [outs_for(wa), outs_for(wb), outs_for(wa), outs_for(wc)]
+    # the 1024-row call has more rows than 2 x CUs: the order pre-pass and the
+    # main kernel are both captured
+    calls = [(sa, oa, la, wa.n_rows, wsa), (sb, ob, lb, wb.n_rows, wsb),
+             (sa, oa, la, wa.n_rows, wsa), (sc, oc, lc, wc.n_rows, wsc)]
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
@@ -356,6 +365,8 @@ def test_graph_capture_and_replay(topk):
                                   where=f"replay {rep} call {j}")
     ri, rv = oracle.topk_ragged(wa.scores, wa.row_offsets, wa.row_lengths, K)
     assert_same_selection(*eager[0], ri, rv, where="eager vs oracle")
+    ri, rv = oracle.topk_ragged(wc.scores, wc.row_offsets, wc.row_lengths, K)
+    assert_same_selection(*eager[3], ri, rv, where="eager vs oracle (1024 rows)")
 
 
 def test_outputs_not_16_byte_aligned(topk):

@@ -63,3 +63,36 @@ def test_plans_are_valid():
         assert seg % 64 == 0 and seg > 0
         assert (P - 1) * seg < L <= P * seg
         assert P <= -(-L // K_SEG_MIN)  # segment p < P has p * kSegMin < L
+
+
+def _header_define(name):
+    import os
+    import re
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    text = open(os.path.join(root, "include", "topk_ragged.h")).read()
+    return int(re.search(rf"#define {name} (0x[0-9A-Fa-f]+|\d+)", text).group(1), 0)
+
+
+def _max_vector_byte_offset(off, beg, end, sh):
+    """The row streaming's largest 16-byte vector offset from its aligned
+    base: nvec = ceil((off + end + sh) / 4) - floor((off + beg + sh) / 4)
+    vectors, the last at byte (nvec - 1) * 16 (sh = the buffer's misalignment
+    in elements, 0..3)."""
+    v0 = (off + beg + sh) >> 2
+    nvec = ((off + end + sh + 3) >> 2) - v0
+    return (nvec - 1) * 16
+
+
+def test_longest_row_keeps_32_bit_vector_offsets():
+    """Rows of up to TOPK_L_MAX elements address every vector of any range of
+    the row with a 32-bit byte offset, for every alignment of the buffer and
+    the row; the first length past a few more elements would wrap."""
+    lmax = _header_define("TOPK_L_MAX")
+    worst = 0
+    for sh in range(4):
+        for off in range(8):
+            worst = max(worst, _max_vector_byte_offset(off, 0, lmax, sh))
+    assert worst < 2**32
+    wraps = max(_max_vector_byte_offset(off, 0, lmax + 4, sh) for sh in range(4) for off in range(8))
+    assert wraps >= 2**32
