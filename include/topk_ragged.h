@@ -193,6 +193,31 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
                    int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                    const topk_ragged_policy *policy, int32_t *row_trace, void *stream);
 
+/* Limits of topk_ragged_noalloc: most rows per call, and most rows a call may
+ * have for its long rows to be split across workgroups (a call of more rows
+ * runs each row on one workgroup, as topk_ragged does above 2 x CUs rows). */
+#define TOPK_NOALLOC_MAX_ROWS 16384
+#define TOPK_NOALLOC_SPLIT_ROWS 64
+
+/* topk_ragged without a workspace argument, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  The library keeps the workspace in a device array of about
+ * 4.5 MB per GPU (header, row-order region, per-row state for
+ * TOPK_NOALLOC_SPLIT_ROWS split rows), held until the process ends; this call
+ * allocates nothing and calls no allocating routine.  The first call on a
+ * device looks up the array's address and enqueues its one-time
+ * initialisation on `stream` ahead of the call.  Arguments, outputs and
+ * results are those of topk_ragged with the per-K policy: the same (index,
+ * value) sets; calls of more than TOPK_NOALLOC_SPLIT_ROWS rows do not split
+ * rows.  Every call on one GPU uses that GPU's array: calls that overlap on
+ * one GPU (concurrent streams or threads) race and must not be made; the
+ * kernels leave the array's state zeroed for the next call.  Returns
+ * TOPK_EWORKSPACE for n_rows > TOPK_NOALLOC_MAX_ROWS, otherwise as
+ * topk_ragged. */
+int topk_ragged_noalloc(const float *scores, const int64_t *row_offsets,
+                        const int32_t *row_lengths, int32_t n_rows, int32_t K, int32_t *out_idx,
+                        float *out_val, void *stream);
+
 /* Copies the workspace's accumulated route counters (see topk_ragged_stats:
  * the per-route row counts behind the recovery rates of Section 6.4) to *out
  * (host memory owned by the caller) and resets them.  Synchronises `stream`:

@@ -32,6 +32,7 @@
 #include <stdint.h>
 #include <climits>
 #include <cstdlib>
+#include <mutex>
 #include <type_traits>
 
 #include "../../include/topk_ragged.h"
@@ -2594,9 +2595,17 @@ extern "C" int topk_ragged_debug_set_timers(uint64_t *buf) {
 }
 #endif
 
-int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
-                   int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
-                   const topk_ragged_policy *policy, int32_t *row_trace, void *stream) {
+} // extern "C"
+
+namespace {
+
+// One call: the order pre-pass when the plan runs each row on one workgroup,
+// then the main kernel.  split_cap: calls of more rows than this are not
+// split (pmax = 1), so that they need no per-row state.
+int launch_call(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
+                int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
+                const topk_ragged_policy *policy, int32_t *row_trace, void *stream,
+                int32_t split_cap) {
     if (n_rows < 0 || K < 1 || K > TOPK_K_MAX) return TOPK_EINVAL;
     if (n_rows == 0) return TOPK_OK;
     if (!scores || !row_offsets || !row_lengths || !out_idx || !out_val || !workspace)
@@ -2609,7 +2618,7 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     DeviceInfo di;
     const int st = device_info(&di);
     if (st != TOPK_OK) return st;
-    const int32_t pmax = plan_pmax(n_rows, di.cus);
+    const int32_t pmax = n_rows > split_cap ? 1 : plan_pmax(n_rows, di.cus);
     if ((int64_t)n_rows * pmax > 0x7FFFFFFFll) return TOPK_EINVAL;
     KArgs a;
     a.scores = scores;
@@ -2651,11 +2660,88 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
 }
 
+} // namespace
+
+extern "C" {
+
+int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
+                   int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
+                   const topk_ragged_policy *policy, int32_t *row_trace, void *stream) {
+    return launch_call(scores, row_offsets, row_lengths, n_rows, K, out_idx, out_val, workspace,
+                       policy, row_trace, stream, INT32_MAX);
+}
+
 int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
                 int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                 void *stream) {
     return topk_ragged_ex(scores, row_offsets, row_lengths, n_rows, K, out_idx, out_val,
                           workspace, nullptr, nullptr, stream);
+}
+
+} // extern "C"
+
+// ------------------------------------------- allocation-free variant ----
+//
+// The workspace of topk_ragged_noalloc: a file-scope device array (one copy
+// per GPU, held until the process ends) laid out like a workspace for
+// TOPK_NOALLOC_MAX_ROWS rows with per-row state for TOPK_NOALLOC_SPLIT_ROWS
+// split rows.  Host code never passes the array's name to a kernel (on the
+// host it is only a stand-in for the symbol): its device address is looked up
+// once per device with hipGetSymbolAddress and kept in g_scratch_ptr.
+constexpr size_t kScratchBytes = kHeaderBytes + kOrderBytes +
+                                 (size_t)TOPK_NOALLOC_SPLIT_ROWS * kRowBlockBytes;
+static_assert(TOPK_NOALLOC_MAX_ROWS <= kOrderMaxRows, "the order region covers every row");
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// The current device's scratch address; on the first call on a device the
+// address is looked up and the header and per-row state are initialised by a
+// kernel enqueued on `stream` (ahead of the call that follows on it).
+int scratch_for_current_device(void **out, hipStream_t stream) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return TOPK_ELAUNCH;
+    if (dev < 0 || dev >= kMaxDevices) return TOPK_EUNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return TOPK_ELAUNCH;
+        WsHeader *hdr = static_cast<WsHeader *>(ptr);
+        char *rows = static_cast<char *>(ptr) + kHeaderBytes + kOrderBytes;
+        hipLaunchKernelGGL(ws_init_kernel, dim3(TOPK_NOALLOC_SPLIT_ROWS), dim3(64), 0, stream, hdr,
+                           rows, (uint32_t)TOPK_NOALLOC_SPLIT_ROWS,
+                           (uint32_t)TOPK_NOALLOC_MAX_ROWS, (uint32_t)kCap);
+        if (hipGetLastError() != hipSuccess) return TOPK_ELAUNCH;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return TOPK_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+int topk_ragged_noalloc(const float *scores, const int64_t *row_offsets,
+                        const int32_t *row_lengths, int32_t n_rows, int32_t K, int32_t *out_idx,
+                        float *out_val, void *stream) {
+    if (n_rows < 0 || K < 1 || K > TOPK_K_MAX) return TOPK_EINVAL;
+    if (n_rows > TOPK_NOALLOC_MAX_ROWS) return TOPK_EWORKSPACE;
+    if (n_rows == 0) return TOPK_OK;
+    if (!scores || !row_offsets || !row_lengths || !out_idx || !out_val) return TOPK_EINVAL;
+    DeviceInfo di;
+    const int st = device_info(&di);
+    if (st != TOPK_OK) return st;
+    void *ws = nullptr;
+    const int sst = scratch_for_current_device(&ws, (hipStream_t)stream);
+    if (sst != TOPK_OK) return sst;
+    return launch_call(scores, row_offsets, row_lengths, n_rows, K, out_idx, out_val, ws, nullptr,
+                       nullptr, stream, TOPK_NOALLOC_SPLIT_ROWS);
 }
 
 int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream) {

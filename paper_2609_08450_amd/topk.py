@@ -86,6 +86,8 @@ def lib():
         L.topk_ragged.restype = ctypes.c_int
         L.topk_ragged_ex.argtypes = [P, P, P, i32, i32, P, P, P, ctypes.POINTER(Policy), P, P]
         L.topk_ragged_ex.restype = ctypes.c_int
+        L.topk_ragged_noalloc.argtypes = [P, P, P, i32, i32, P, P, P]
+        L.topk_ragged_noalloc.restype = ctypes.c_int
         L.topk_ragged_workspace_size.argtypes = [i32, i32]
         L.topk_ragged_workspace_size.restype = ctypes.c_size_t
         L.topk_ragged_workspace_init.argtypes = [P, ctypes.c_size_t, i32, i32, P]
@@ -190,6 +192,17 @@ def topk_ragged_ex(scores, row_offsets, row_lengths, n_rows: int, K: int, out_id
                                 ctypes.byref(policy) if policy is not None else None,
                                 _ptr(row_trace, torch.int32, "row_trace"), _stream(stream)),
            "topk_ragged_ex")
+
+
+def topk_ragged_noalloc(scores, row_offsets, row_lengths, n_rows: int, K: int, out_idx, out_val,
+                        stream=None) -> None:
+    """Forwards to topk_ragged_noalloc() (the library's own workspace)."""
+    _check(lib().topk_ragged_noalloc(_ptr(scores, torch.float32, "scores"),
+                                     _ptr(row_offsets, torch.int64, "row_offsets"),
+                                     _ptr(row_lengths, torch.int32, "row_lengths"), n_rows, K,
+                                     _ptr(out_idx, torch.int32, "out_idx"),
+                                     _ptr(out_val, torch.float32, "out_val"), _stream(stream)),
+           "topk_ragged_noalloc")
 
 
 def read_stats(workspace, stream=None) -> dict:

@@ -63,6 +63,12 @@ def test_host_argument_checks(lib):
     assert lib.topk_ragged_debug_coarse(n, -1, n, n) == -1
     assert lib.topk_ragged_debug_coarse(n, 0, n, n) == 0
     assert lib.topk_ragged_status_str(-1) == b"invalid argument"
+    # the allocation-free call: its row limit and scalar checks come first
+    assert lib.topk_ragged_noalloc(n, n, n, 16385, 2048, n, n, n) == -4
+    assert lib.topk_ragged_noalloc(n, n, n, 0, 2048, n, n, n) == 0
+    assert lib.topk_ragged_noalloc(n, n, n, -1, 2048, n, n, n) == -1
+    assert lib.topk_ragged_noalloc(n, n, n, 4, 0, n, n, n) == -1
+    assert lib.topk_ragged_noalloc(n, n, n, 4, 2048, n, n, n) == -1       # null pointers
     del dummy, bad
 
 
