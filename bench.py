@@ -9,7 +9,10 @@ back-to-back on one stream.  HIP events on that stream bracket exactly
 `--steps` calls after exactly `--warmup` untimed ones; a busy kernel queued
 just before the first event keeps the host's graph launch out of the timed
 region.  `--rounds` more rounds of about 100 calls are timed separately and
-their median is reported beside the main figure.
+their median is reported beside the main figure.  The line also carries the
+time of the library's read-only ceiling kernel over the same rows (every valid
+score read once with the same work items and loads, no selection): what a
+single launch of this geometry can reach at all.
 
 Metric: effective score-read bandwidth = 4 B x sum(L) per call / time per
 call, the algorithmic bytes of an exact selector (one complete read of every
@@ -219,14 +222,16 @@ def upload_graph(g, stream) -> bool:
 
 
 def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0, rounds=0,
-               round_calls=100):
+               round_calls=100, ceiling=False):
     """Times exactly `steps` topk_ragged calls on workload wl (policy None =
     the production call) over rotated device copies, captured in HIP graphs
     and replayed on one stream between HIP events on that stream, after
     exactly `warmup` untimed calls.  A busy kernel is queued ahead of the
     first event so that the host's graph launch is not inside the timed
     region.  With rounds > 0, also times that many separate rounds of about
-    round_calls calls each and reports their median.  Returns a dict."""
+    round_calls calls each and reports their median.  ceiling: time the
+    library's read-only ceiling kernel over the same rows instead of the
+    selector.  Returns a dict."""
     import torch
 
     from paper_2609_08450_amd import topk
@@ -245,11 +250,14 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0, rounds
         lens = torch.from_numpy(wl.row_lengths).to(dev)
         out_idx = torch.empty((n, K), dtype=torch.int32, device=dev)
         out_val = torch.empty((n, K), dtype=torch.float32, device=dev)
+        out_max = torch.zeros(n, dtype=torch.int32, device=dev)
         ws = topk.alloc_workspace(n, K, dev, stream)
     stream.synchronize()
 
     def call(i, s):
-        if policy is None:
+        if ceiling:
+            topk.debug_read_ceiling(bufs[i % copies], offs, lens, n, K, out_max, s)
+        elif policy is None:
             topk.topk_ragged(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws, s)
         else:
             topk.topk_ragged_ex(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws,
@@ -312,10 +320,11 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0, rounds
                          "ms_per_call_min": per[0], "ms_per_call_max": per[-1]}
 
     # outside the timed region: route counts of one call
-    topk.read_stats(ws, stream)
-    with torch.cuda.stream(stream):
-        call(0, stream)
-    out["routes"] = topk.read_stats(ws, stream)
+    if not ceiling:
+        topk.read_stats(ws, stream)
+        with torch.cuda.stream(stream):
+            call(0, stream)
+        out["routes"] = topk.read_stats(ws, stream)
     del bufs, g_main, g_tail
     torch.cuda.synchronize()
     return out
@@ -418,6 +427,8 @@ def main():
                     help="after the timed steps, this many separately timed rounds of about 100 "
                          "calls (median reported); 0 = none")
     ap.add_argument("--no-rotate", action="store_true", help="reuse one copy (cache-resident input)")
+    ap.add_argument("--no-ceiling", dest="ceiling", action="store_false",
+                    help="skip timing the read-only ceiling kernel over the same rows")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of all-core oracle time (plus a third of it on one thread); "
                          "0 = skip")
@@ -498,6 +509,17 @@ def main():
                             "us_per_call_min": round(rd["ms_per_call_min"] * 1e3, 3),
                             "us_per_call_max": round(rd["ms_per_call_max"] * 1e3, 3),
                             "gbs_median": round(alg_bytes / (rd["ms_per_call_median"] * 1e-3) / 1e9, 2)}
+    if args.ceiling:
+        c = time_calls(wl, None, args.steps, args.warmup, not args.no_rotate, args.calls_per_graph,
+                       rounds=args.rounds, ceiling=True)
+        cms = c["rounds"]["ms_per_call_median"] if "rounds" in c else c["ms_per_call"]
+        sms = t["rounds"]["ms_per_call_median"] if "rounds" in t else ms_per_step
+        cgbs = alg_bytes / (cms * 1e-3) / 1e9
+        result["ceiling"] = {"kernel": "read_ceiling_kernel",
+                             "what": "every valid score read once, same work items and loads",
+                             "us_per_call": round(cms * 1e3, 3), "gbs": round(cgbs, 2),
+                             "frac_of_hbm_peak": round(cgbs / HBM_PEAK_GBS, 4),
+                             "selector_frac_of_ceiling": round(cms / sms, 4)}
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     else:

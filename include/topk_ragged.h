@@ -233,6 +233,20 @@ int topk_ragged_read_stats(void *workspace, topk_ragged_stats *out, void *stream
 int topk_ragged_debug_coarse(const float *x, int64_t n, uint16_t *out_c, void *stream);
 int topk_ragged_debug_cutoffs(uint32_t *out_cut, void *stream);
 
+/* Read-only ceiling of a call, for measurement: the work items topk_ragged
+ * would launch for these rows and this K (the same split plan, per-K policy,
+ * one workgroup for every row it does not split) stream every valid score
+ * once with the same 16-byte loads and keep only the row's largest score.
+ * Algorithmic bytes are the operator's own (one read of every valid score,
+ * R_eq = 1 of Section 2.1, "Why long rows are expensive"), so the time of
+ * this call bounds what the selector can reach in that geometry.  out_max: device, uint32
+ * [n_rows], caller-owned, zeroed by the caller; receives the order-preserving
+ * key of each row's largest score (0 for an empty row).  Same argument
+ * errors as topk_ragged; no workspace. */
+int topk_ragged_debug_read_ceiling(const float *scores, const int64_t *row_offsets,
+                                   const int32_t *row_lengths, int32_t n_rows, int32_t K,
+                                   uint32_t *out_max, void *stream);
+
 /* For tests of the split-row wait (Section 4.5 mapping): the number of polls a
  * segment makes for segment 0's published boundaries before it builds the
  * view itself (counted in topk_ragged_stats.wait_fallback), for the calls

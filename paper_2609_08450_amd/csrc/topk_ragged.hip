@@ -1424,7 +1424,7 @@ __device__ __forceinline__ uint32_t udiv32(uint32_t x, uint32_t y) {
 // splittable call computes it to size its row's segments); len0 is this
 // thread's first term, lens[threadIdx.x] (0 past the last row), loaded
 // by the caller ahead of time.  Ends with a barrier.
-__device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm, int32_t len0) {
+__device__ __forceinline__ int64_t block_total_length(const KArgs a, int64_t *lsum, int32_t len0) {
     uint64_t s = (uint64_t)max(len0, 0);
     for (int t = threadIdx.x + kBlock; t < a.n_rows; t += kBlock) s += (uint64_t)max(a.lens[t], 0);
     // s < 2^53: wave sums of its bits [0,16), [16,32), [32,53) each fit 32 bits
@@ -1432,12 +1432,39 @@ __device__ __forceinline__ int64_t block_total_length(const KArgs a, Smem &sm, i
     const uint32_t mid = wave_incl_scan((uint32_t)(s >> 16) & 0xFFFFu);
     const uint32_t hi = wave_incl_scan((uint32_t)(s >> 32));
     if (lane_id() == 63)
-        sm.lsum[threadIdx.x >> 6] = (int64_t)lo + ((int64_t)mid << 16) + ((int64_t)hi << 32);
+        lsum[threadIdx.x >> 6] = (int64_t)lo + ((int64_t)mid << 16) + ((int64_t)hi << 32);
     __syncthreads();
     int64_t tot = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; w++) tot += sm.lsum[w];
+    for (int w = 0; w < kWaves; w++) tot += lsum[w];
     return tot;
+}
+
+// The split plan of a row of length L (KV-split mapping, Section 4.5): when
+// rows may be split, the row is cut into P0 = min(pmax, ceil(L / target))
+// pieces of equal length rounded up to 64 elements, target = max(kSegMin,
+// sum(L) / items), so that the call has at most about seg_items work items;
+// P <= P0 <= ceil(L / kSegMin).  total = sum(L) of the call.  Every segment
+// of the row computes the same plan.
+__device__ __forceinline__ void segment_plan(const KArgs a, int64_t total, int64_t L, int64_t &P,
+                                             int64_t &seg) {
+    // (a call of more rows than items cuts only the rows longer than the
+    // mean, in two: the longest rows no longer bound the call)
+    const int64_t items = a.n_rows > a.seg_items ? a.n_rows
+                        : a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
+                                                     : (a.seg_items + 1) / 2;
+    // Divisions in FP64 (a few instructions, where 64-bit integer division
+    // takes hundreds).  target and P0 may be off by one after rounding: any
+    // target >= kSegMin and any P0 in [1, ceil(L / kSegMin)] make a valid
+    // plan, and every segment of the row computes the same one.  seg and P
+    // are exact (udiv32).
+    const double tq = ceil((double)total / (double)items);
+    const uint32_t target = (uint32_t)fmax((double)kSegMin, fmin(tq, 2147483648.0));
+    const uint32_t L32 = (uint32_t)L;
+    const uint32_t P0 = min((uint32_t)a.pmax, (uint32_t)ceil((double)L32 / (double)target));
+    const uint32_t seg32 = (udiv32(L32 + P0 - 1u, P0) + 63u) & ~63u;
+    seg = seg32;
+    P = udiv32(L32 + seg32 - 1u, seg32);
 }
 
 // Phase 1 in two halves.  phase1_issue loads the first kP1 view samples of
@@ -1998,31 +2025,10 @@ topk_ragged_kernel(KArgs a) {
         float xs[kP1];
         const bool big_view = nv >= kCoopView && a.pmax > 1;
         if (p == 0 && !big_view) phase1_issue(a, r, row, L, xs);
-        // Segments: when rows may be split, a row is cut into P0 =
-        // min(pmax, ceil(L / target)) pieces of equal length rounded up to 64
-        // elements, target = max(kSegMin, sum(L) / items), so that the call
-        // has at most about seg_items work items.  P <= P0 <= ceil(L / kSegMin).
+        // Segments (segment_plan) when rows may be split.
         int64_t P = 1, seg = L;
-        if (a.pmax > 1) {
-            const int64_t total = block_total_length(a, sm, tid < a.n_rows ? len0_raw : 0);
-            // (a call of more rows than items cuts only the rows longer than
-            // the mean, in two: the longest rows no longer bound the call)
-            const int64_t items = a.n_rows > a.seg_items ? a.n_rows
-                                : a.seg_items > 2 * a.n_rows ? a.seg_items - a.n_rows
-                                                             : (a.seg_items + 1) / 2;
-            // Divisions in FP64 (a few instructions, where 64-bit integer
-            // division takes hundreds).  target and P0 may be off by one
-            // after rounding: any target >= kSegMin and any P0 in
-            // [1, ceil(L / kSegMin)] make a valid plan, and every segment of
-            // the row computes the same one.  seg and P are exact (udiv32).
-            const double tq = ceil((double)total / (double)items);
-            const uint32_t target = (uint32_t)fmax((double)kSegMin, fmin(tq, 2147483648.0));
-            const uint32_t L32 = (uint32_t)L;
-            const uint32_t P0 = min((uint32_t)a.pmax, (uint32_t)ceil((double)L32 / (double)target));
-            const uint32_t seg32 = (udiv32(L32 + P0 - 1u, P0) + 63u) & ~63u;
-            seg = seg32;
-            P = udiv32(L32 + seg32 - 1u, seg32);
-        }
+        if (a.pmax > 1)
+            segment_plan(a, block_total_length(a, sm.lsum, tid < a.n_rows ? len0_raw : 0), L, P, seg);
         if (p >= P) return;
         split = P > 1;
         const int32_t beg = (int32_t)(p * seg);
@@ -2431,6 +2437,59 @@ __global__ void debug_cutoff_kernel(uint32_t *out) {
 
 // ------------------------------------------------------------- host ----
 
+// Read-only ceiling of a call: the same work items as topk_ragged_kernel
+// (rows that the main kernel splits are cut by the same plan, every other row
+// is read by one workgroup) stream every valid score once with the same
+// loads (two chunks of 16-byte non-temporal loads in flight per thread) and
+// keep only the largest ascending key, which one atomic per workgroup adds
+// into out_max[r] (atomics on one address queue: one per wave made the
+// long-split batch's ceiling 1.5 times slower than the selector itself).  It
+// measures what reading the call's rows costs in this launch geometry, with
+// none of the selection.
+__global__ __launch_bounds__(kBlock) void read_ceiling_kernel(KArgs a, uint32_t *out_max) {
+    __shared__ int64_t lsum[kWaves];
+    __shared__ uint32_t wmax[kWaves];
+    const int tid = threadIdx.x;
+    const int p = blockIdx.x / a.n_rows;
+    const int r = blockIdx.x - p * a.n_rows;
+    const int32_t len_r = a.lens[r];
+    const int64_t off = a.offs[r];
+    const int32_t len0 = a.lens[min(tid, a.n_rows - 1)];
+    const int64_t L = (int64_t)max(len_r, 0);
+    const bool sampled = L > a.K && L >= a.l_samp_min &&
+                         view_size(L, view_phase(r, a.s_log2), a.s_log2) >= a.q1;
+    if (!sampled && p > 0) return;
+    int64_t P = 1, seg = L;
+    if (sampled && a.pmax > 1) {
+        if ((int64_t)p * kSegMin >= L) return;
+        segment_plan(a, block_total_length(a, lsum, tid < a.n_rows ? len0 : 0), L, P, seg);
+    }
+    if (p >= P) return;
+    const int32_t beg = (int32_t)(p * seg);
+    const int32_t end = (int32_t)min(L, p * seg + seg);
+    uint32_t mx = 0;
+    stream_row<true>(a.scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                                   int32_t hi, bool, int32_t mv) {
+#pragma unroll
+        for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+                const uint32_t u = asc_key(fbits(x[m][c]));
+                mx = in_window(i0[m] + c, lo, hi) ? max(mx, u) : mx;
+            }
+        }
+    });
+    mx = wave_max_to63(mx);
+    if (lane_id() == 63) wmax[tid >> 6] = mx;
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; w++) m = max(m, wmax[w]);
+        atomicMax(&out_max[r], m);
+    }
+}
+
 struct DeviceInfo {
     int cus = 0;
     bool ok = false;
@@ -2774,6 +2833,38 @@ int topk_ragged_debug_coarse(const float *x, int64_t n, uint16_t *out_c, void *s
     if (blocks > 0x7FFFFFFFll) return TOPK_EINVAL;
     hipLaunchKernelGGL(debug_coarse_kernel, dim3((unsigned)blocks), dim3(256), 0,
                        (hipStream_t)stream, x, n, out_c);
+    return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
+}
+
+int topk_ragged_debug_read_ceiling(const float *scores, const int64_t *row_offsets,
+                                   const int32_t *row_lengths, int32_t n_rows, int32_t K,
+                                   uint32_t *out_max, void *stream) {
+    if (n_rows < 0 || K < 1 || K > TOPK_K_MAX) return TOPK_EINVAL;
+    if (n_rows == 0) return TOPK_OK;
+    if (!scores || !row_offsets || !row_lengths || !out_max) return TOPK_EINVAL;
+    DeviceInfo di;
+    const int st = device_info(&di);
+    if (st != TOPK_OK) return st;
+    const int32_t pmax = plan_pmax(n_rows, di.cus);
+    if ((int64_t)n_rows * pmax > 0x7FFFFFFFll) return TOPK_EINVAL;
+    const topk_ragged_policy pol = policy_for_k(K);
+    KArgs a = {};
+    a.scores = scores;
+    a.offs = row_offsets;
+    a.lens = row_lengths;
+    a.n_rows = n_rows;
+    a.K = K;
+    a.pmax = pmax;
+    a.seg_items = plan_items(di.cus);
+    a.s_log2 = pol.s_log2;
+    a.q0 = sample_rank(K, pol.rho_num, pol.rho_den, pol.s_log2);
+    a.q1 = sample_rank(K, pol.rho1_num, pol.rho1_den, pol.s_log2);
+    if (a.q1 < a.q0) a.q1 = a.q0;
+    const int64_t floor_k = -(int64_t)pol.l_samp_min * K;
+    a.l_samp_min = pol.l_samp_min >= 0 ? pol.l_samp_min
+                                       : (int32_t)(floor_k < 0x7FFFFFFF ? floor_k : 0x7FFFFFFF);
+    hipLaunchKernelGGL(read_ceiling_kernel, dim3((unsigned)(n_rows * pmax)), dim3(kBlock), 0,
+                       (hipStream_t)stream, a, out_max);
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
 }
 

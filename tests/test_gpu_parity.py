@@ -538,3 +538,24 @@ def test_segments_that_stop_waiting_build_the_view(topk):
         topk.debug_set_spin_limit(0)
     say("routes", st)
     assert st["wait_fallback"] > 0
+
+
+@pytest.mark.parametrize("cfg", [2, 5])
+def test_read_ceiling_reads_every_score(topk, cfg):
+    """The read-only ceiling kernel (the measurement's bound) visits every
+    valid score of every row once: its per-row maximum key equals numpy's."""
+    import torch
+
+    wl = W.make(cfg)
+    say("read ceiling", wl.name)
+    s, o, l = device_arrays(wl)
+    out = torch.zeros(wl.n_rows, dtype=torch.int32, device="cuda")
+    topk.debug_read_ceiling(s, o, l, wl.n_rows, wl.K, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32)
+    want = np.zeros(wl.n_rows, np.uint32)
+    for r in range(wl.n_rows):
+        x = wl.row(r)
+        if x.size:
+            want[r] = oracle.asc32(x.view(np.uint32)).max()
+    assert np.array_equal(got, want)
