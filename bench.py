@@ -38,7 +38,11 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 MALL_BYTES = 256 << 20
 ROTATE_MIN_BYTES = 512 << 20
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_08450_amd", "csrc", "topk_ragged.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode.json")
+WORKLOAD_NAMES = {1: "tiny", 2: "decode", 3: "chunked_prefill", 4: "long_split", 5: "adversarial"}
+
+
+def traffic_file(config: int) -> str:
+    return os.path.join(ROOT, "profiles", f"traffic_{WORKLOAD_NAMES[config]}.json")
 
 
 def kernel_source_hash() -> str:
@@ -50,7 +54,7 @@ def measured_traffic(config: int):
     """HBM bytes per launch from the committed rocprofv3 counter runs, or None
     when they are missing or were taken on a different kernel source."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(traffic_file(config)) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
@@ -439,7 +443,7 @@ def main():
                          "counter CSVs from rocprofv3 --pmc; writes the traffic file and exits")
     ap.add_argument("--copy-mib", type=int, default=1024, help="size of the calibration copy")
     ap.add_argument("--traffic-out", default=None,
-                    help="where --traffic-summary writes (default: the decode traffic file "
+                    help="where --traffic-summary writes (default: the config's traffic file "
                          "that the bench line reports)")
     ap.add_argument("--ablation", choices=ABLATIONS, default=None,
                     help="instead of the bench line, one JSON line per policy variant (the "
@@ -448,7 +452,7 @@ def main():
 
     if args.traffic_summary:
         traffic_summary(args.traffic_summary, args.config, args.copy_mib,
-                        args.traffic_out or TRAFFIC_FILE)
+                        args.traffic_out or traffic_file(args.config))
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
