@@ -58,6 +58,7 @@ constexpr int kMaxSplit = 64;               // most segments per row
 constexpr int kSegMin = 8192;               // shortest segment, elements
 constexpr uint32_t kMagic = 0x544F504Bu;    // workspace header tag
 constexpr int kSpinLimit = 1 << 15;         // polls before recomputing the view
+constexpr int kSpinMicros = 100;            // and the longest wait for the boundaries
 constexpr size_t kHeaderBytes = 1024;
 constexpr size_t kRowStateBytes = 256;
 constexpr uintptr_t kWorkspaceAlign = 256; // 64-bit atomics and 16-byte header loads
@@ -129,6 +130,7 @@ struct KArgs {
     int32_t l_samp_min;
     int32_t cap;
     int32_t spin_limit; // polls of the boundary word before a segment builds the view itself
+    uint32_t spin_ticks; // and the most constant-rate clock ticks it waits for them
 #ifdef TOPK_PHASE_TIMERS
     uint64_t *timers; // 32 words per workgroup, see PHASE_MARK
 #endif
@@ -238,27 +240,6 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
     return v;
 }
 
-// Wave64 OR / AND of a value; the result is valid in lane 63.
-__device__ __forceinline__ uint32_t wave_or_to63(uint32_t v) {
-    v |= __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xf, 0xf, false);
-    v |= __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xf, 0xf, false);
-    v |= __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xf, 0xf, false);
-    v |= __builtin_amdgcn_update_dpp(0u, v, 0x118, 0xf, 0xf, false);
-    v |= __builtin_amdgcn_update_dpp(0u, v, 0x142, 0xa, 0xf, false);
-    v |= __builtin_amdgcn_update_dpp(0u, v, 0x143, 0xc, 0xf, false);
-    return v;
-}
-
-__device__ __forceinline__ uint32_t wave_and_to63(uint32_t v) {
-    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x111, 0xf, 0xf, false);
-    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x112, 0xf, 0xf, false);
-    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x114, 0xf, 0xf, false);
-    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x118, 0xf, 0xf, false);
-    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x142, 0xa, 0xf, false);
-    v &= __builtin_amdgcn_update_dpp(~0u, v, 0x143, 0xc, 0xf, false);
-    return v;
-}
-
 // Wave64 minimum / maximum; the result is valid in lane 63.
 __device__ __forceinline__ uint32_t wave_min_to63(uint32_t v) {
     v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(~0u, v, 0x111, 0xf, 0xf, false));
@@ -278,28 +259,6 @@ __device__ __forceinline__ uint32_t wave_max_to63(uint32_t v) {
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x142, 0xa, 0xf, false));
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0u, v, 0x143, 0xc, 0xf, false));
     return v;
-}
-
-// Wave-aggregated append: every lane of the wave must call it.  Returns the
-// slot of this lane's item (meaningful only where pred is true).
-__device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t *ctr) {
-    const uint64_t m = __ballot(pred);
-    if (m == 0) return 0;
-    const uint32_t pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    uint32_t base = 0;
-    if (lane_id() == 0) base = atomicAdd(ctr, (uint32_t)__popcll(m));
-    return __builtin_amdgcn_readfirstlane(base) + pre;
-}
-
-// Wave-aggregated append for a ballot mask already computed by the caller:
-// one LDS atomic per wave.  Every lane of the wave must call it.
-__device__ __forceinline__ uint32_t wave_append_bits(uint64_t m, uint32_t *ctr) {
-    const uint32_t pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    uint32_t base = 0;
-    if (lane_id() == 0) base = atomicAdd(ctr, (uint32_t)__popcll(m));
-    return __builtin_amdgcn_readfirstlane(base) + pre;
 }
 
 struct Find {
@@ -1791,7 +1750,7 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
                                             uint32_t ngroups, const uint32_t (&vi)[kPer],
                                             const uint32_t (&vk)[kPer]) {
     const int tid = threadIdx.x;
-    const uint32_t lane = (uint32_t)lane_id(), w8 = (uint32_t)tid >> 6;
+    const uint32_t lane = (uint32_t)lane_id();
     const uint32_t K = (uint32_t)a.K, cap = (uint32_t)a.cap;
     uint32_t route, kmin, n_live;
     if (C0 >= K && C0 <= cap) {
@@ -2042,12 +2001,17 @@ topk_ragged_kernel(KArgs a) {
             phase1_issue(a, r, row, L, xs); // not split: the whole view, after the plan
         }
         // Phase 2 over this segment: certify against cut0 and keep A(tau1).
-        // The endpoints come from segment 0, which publishes tau0 and tau1 in
-        // one agent-scope atomic word (the endpoints follow from the bins);
-        // other segments poll for it with their first chunk in flight and
-        // build the view themselves if it does not come within the spin
-        // limit.  Segment 0 never waits for another segment, and every
-        // segment 0 is dispatched before any other segment, so the wait ends.
+        // The endpoints come from segment 0 (or, for a shared view, from the
+        // last segment to add its part), which publishes tau0 and tau1 in one
+        // agent-scope atomic word (the endpoints follow from the bins); the
+        // other segments poll for it with their first chunk in flight.  The
+        // wait is bounded, by a poll count and by spin_ticks of the
+        // constant-rate clock: after either, the segment builds the whole
+        // view itself (the same boundaries).  That bound is what guarantees
+        // progress: a row's segments are normally resident together (a call
+        // has fewer work items than resident workgroups), but another kernel
+        // sharing the GPU can keep the publishing segment from running, and
+        // with a shared view any segment may wait for one dispatched after it.
         PHASE_MARK(a, 16);
         phase2_collect(sm, a.scores, off, beg, end, [&]() {
             bool have = false; // endpoints in sm
@@ -2061,9 +2025,10 @@ topk_ragged_kernel(KArgs a) {
             if (!have) {
                 if (tid == 0) {
                     uint32_t v = 0;
+                    const uint64_t t_wait = wall_clock64();
                     for (int spin = 0; spin < a.spin_limit; spin++) {
                         v = __hip_atomic_load(&rs->taus, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        if (v & 0x80000000u) break;
+                        if ((v & 0x80000000u) || wall_clock64() - t_wait > a.spin_ticks) break;
                         __builtin_amdgcn_s_sleep(1);
                     }
                     PHASE_MARK(a, 20);
@@ -2492,6 +2457,7 @@ __global__ __launch_bounds__(kBlock) void read_ceiling_kernel(KArgs a, uint32_t 
 
 struct DeviceInfo {
     int cus = 0;
+    int clock_khz = 0; // rate of the constant-rate clock (wall_clock64)
     bool ok = false;
 };
 
@@ -2504,6 +2470,11 @@ int device_info(DeviceInfo *di) {
         hipDeviceProp_t prop;
         if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return TOPK_ELAUNCH;
         cached.cus = prop.multiProcessorCount;
+        int khz = 0;
+        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+            khz <= 0)
+            khz = 100000; // 100 MHz, the rate on gfx9 parts
+        cached.clock_khz = khz;
         cached.ok = (prop.gcnArchName[0] == 'g' && prop.gcnArchName[3] == '9' &&
                      prop.gcnArchName[4] == '5' && prop.gcnArchName[5] == '0');
         cached_dev = dev;
@@ -2705,6 +2676,7 @@ int launch_call(const float *scores, const int64_t *row_offsets, const int32_t *
                                        : (int32_t)(floor_k < 0x7FFFFFFF ? floor_k : 0x7FFFFFFF);
     a.cap = pol.cap;
     a.spin_limit = g_spin_limit > 0 ? g_spin_limit : kSpinLimit;
+    a.spin_ticks = (uint32_t)((int64_t)kSpinMicros * di.clock_khz / 1000);
     if (pmax == 1 && n_rows <= kOrderMaxRows) {
         // more rows than resident workgroups: longest rows first, so that
         // the last to start is short

@@ -411,15 +411,21 @@ def test_shared_view_rows(topk):
 
 
 @pytest.mark.parametrize("K", [1, 7, 100, 256, 383, 384, 512, 1000, 1024, 1600, 2047, 2500,
-                               2560, 3000, 4096, 4351, 4352, 6000])
+                               2560, 3000, 4096, 4351, 4352, 6000, 8192, 16384])
 def test_parity_per_k_policy(topk, K):
     """Calls without a policy use the per-K constants (topk_ragged_policy_for_k):
     decode-mixture rows around the sampling floor and up to 131072 elements,
-    selections and per-row routes against the oracle under that policy."""
+    selections and per-row routes against the oracle under that policy.  From
+    K = 8192 (past the on-chip frontier) a row of 200000 equal values is
+    added: its boundary bin holds more entries than the frontier, so the
+    re-read path runs at large K too."""
     rng = np.random.default_rng(1000 + K)
     lens = sorted({max(1, K - 1), K + 1, 4 * K - 1, 4 * K, 4 * K + 7, 10 * K + 3, 16384, 40000,
                    90001, 131072})
     rows = [W.decode_mixture_row(rng, int(L)).astype(np.float32) for L in lens]
+    if K >= 8192:
+        rows.append(np.full(200000, 0.5, np.float32))
+        lens.append(200000)
     lens = np.array(lens, np.int32)
     offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
     wl = W.Workload(f"per-K policy K={K}", np.concatenate(rows), offs, lens, K, "")
@@ -427,6 +433,8 @@ def test_parity_per_k_policy(topk, K):
     say("routes", st)
     if K >= 4352:
         assert st["primary"] + st["band"] == 0
+    if K >= 8192:
+        assert st["reread"] >= 1
 
 
 def test_single_workgroup_rows_with_an_overflowed_region(topk):
