@@ -260,7 +260,7 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0, rounds
 
     def call(i, s):
         if ceiling:
-            topk.debug_read_ceiling(bufs[i % copies], offs, lens, n, K, out_max, s)
+            topk.debug_read_ceiling(bufs[i % copies], offs, lens, n, K, out_max, ws, s)
         elif policy is None:
             topk.topk_ragged(bufs[i % copies], offs, lens, n, K, out_idx, out_val, ws, s)
         else:

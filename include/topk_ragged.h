@@ -241,11 +241,14 @@ int topk_ragged_debug_cutoffs(uint32_t *out_cut, void *stream);
  * R_eq = 1 of Section 2.1, "Why long rows are expensive"), so the time of
  * this call bounds what the selector can reach in that geometry.  out_max: device, uint32
  * [n_rows], caller-owned, zeroed by the caller; receives the order-preserving
- * key of each row's largest score (0 for an empty row).  Same argument
- * errors as topk_ragged; no workspace. */
+ * key of each row's largest score (0 for an empty row).  workspace: an
+ * initialised workspace for at least n_rows rows (as for topk_ragged), whose
+ * item-table region receives the work items of a call with more rows than
+ * resident workgroups; no other part of it is written.  Same argument errors
+ * as topk_ragged. */
 int topk_ragged_debug_read_ceiling(const float *scores, const int64_t *row_offsets,
                                    const int32_t *row_lengths, int32_t n_rows, int32_t K,
-                                   uint32_t *out_max, void *stream);
+                                   uint32_t *out_max, void *workspace, void *stream);
 
 /* For tests of the split-row wait (Section 4.5 mapping): the number of polls a
  * segment makes for segment 0's published boundaries before it builds the

@@ -62,7 +62,12 @@ constexpr int kSpinMicros = 100;            // and the longest wait for the boun
 constexpr size_t kHeaderBytes = 1024;
 constexpr size_t kRowStateBytes = 256;
 constexpr uintptr_t kWorkspaceAlign = 256; // 64-bit atomics and 16-byte header loads
-constexpr size_t kViewHistBytes = kBins * sizeof(uint32_t); // a split row's merged view histogram
+// a split row's merged view histogram; its merged coarse histogram of the
+// segments whose candidates overflowed has the same size and sits in a
+// region of its own after the row blocks (so that the blocks keep their
+// 64 KB + 256 B stride: with the histogram inside them the decode batch ran
+// 10 % slower)
+constexpr size_t kViewHistBytes = kBins * sizeof(uint32_t);
 constexpr size_t kRowBlockBytes = kRowStateBytes + kViewHistBytes + 2 * kFront * sizeof(uint32_t);
 // Views of at least this many samples are shared by a split row's segments
 // (each histograms the samples inside its own range and the histograms are
@@ -71,32 +76,49 @@ constexpr size_t kRowBlockBytes = kRowStateBytes + kViewHistBytes + 2 * kFront *
 constexpr int64_t kCoopView = 4096;
 // Most segments a row may have for its segments to publish per wave.
 constexpr int64_t kWavePublishMaxSegs = 16;
-// Calls whose rows each take one workgroup (more rows than can be resident)
-// run their rows longest first: a pre-pass writes the order, one 16-byte
-// entry (row, length, offset) per row, into a fixed region after the header,
-// for calls of up to kOrderMaxRows rows.
+// Calls with more rows than can be resident run their rows longest first: a
+// pre-pass writes the work items, one 16-byte entry (row, segment, segments,
+// length, offset, row-state slot) each, into a fixed region after the header,
+// for calls of up to kOrderMaxRows rows.  Among the kOrderBlock longest rows,
+// those much longer than the call's mean work per resident workgroup are cut
+// into segments, at most kOrderExtra more items per call.
 constexpr int kOrderMaxRows = 16384;
-constexpr size_t kOrderBytes = (size_t)kOrderMaxRows * 16;
+constexpr int kOrderExtra = 1024;
+constexpr size_t kOrderBytes = (size_t)(kOrderMaxRows + kOrderExtra) * 16;
 constexpr int kOrderBlock = 1024;
 constexpr int kOrderPer = kOrderMaxRows / kOrderBlock;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-// Per-row state of a split row.  Row r of a split call owns the workspace
-// block at kHeaderBytes + kOrderBytes + r * kRowBlockBytes: this state, padded to 256
-// bytes, the 2048-bin view histogram that segments sharing the view add
+// Per-row state of a split row.  The row in slot k (its index r when every
+// row may be split, else the slot the item table gives it) owns the workspace
+// block at kHeaderBytes + kOrderBytes + k * kRowBlockBytes: this state, padded
+// to 256 bytes, the 2048-bin view histogram that segments sharing the view add
 // into, then kFront candidates as 64-bit (index | FP32 bits << 32) words
-// (the segments' A(tau1) entries, concatenated).  Every field and entry is
-// written and read with agent-scope atomic accesses (see the arrive step).
+// (the segments' A(tau1) entries, concatenated); and the 2048-bin coarse
+// histogram at kHeaderBytes + kOrderBytes + split_rows * kRowBlockBytes +
+// k * kViewHistBytes.  Every field and entry is written and read with
+// agent-scope atomic accesses (see the arrive step).
 struct RowState {
     uint64_t sa;         // entries reserved in the candidate buffer (low 32
                          // bits) | segments done with Phase 2 << 32: the last
                          // arrival's atomic returns the final reserved count
     uint64_t counts;     // C(tau1) | C(tau0) << 32 of the row (exact)
     uint32_t taus;       // segment 0's tau0 | tau1 << 16 | 1 << 31 once known
-    uint32_t incomplete; // a segment could not keep all of its A(tau1)
+    uint32_t incomplete; // a segment could not keep all of its A(tau1): with
+                         // per-wave publishing 1, else the number of such
+                         // segments (each adds its coarse histogram)
     uint32_t amax;       // largest ascending key among the stored entries
     uint32_t varrive;    // segments that have added their part of a shared view
+    // The split exact route (segments that added a histogram wait for the
+    // finisher's tau_star, classify their own ranges and arrive again):
+    uint32_t xtau;       // 1 << 31 | abandoned << 30 | arrivals expected << 11 | tau_star
+    uint32_t ocnt;       // outputs reserved (entries with c < tau_star)
+    uint32_t qcnt;       // kept entries (c == tau_star) reserved in the candidate buffer
+    uint32_t arrive2;    // second arrivals
+    uint32_t xbelow;     // |E0| and |Q0| of the row, for the last arrival
+    uint32_t xeq;
+    uint64_t xmask;      // segments whose ranges the last arrival classifies
 };
 
 // Workspace header (first kHeaderBytes of the workspace).
@@ -383,6 +405,7 @@ struct alignas(16) Smem {
     uint32_t base;
     int64_t lsum[kWaves]; // per-wave partial sums of the row lengths
     uint32_t amax;        // largest ascending key among the stored entries
+    uint32_t xword;       // split exact route: the route word a waiting segment saw
 };
 
 __device__ __forceinline__ void clear_hist(Smem &sm) {
@@ -1203,10 +1226,11 @@ __device__ __forceinline__ void coarse_hist_chunk(Smem &sm, const f4 *x, const i
     }
 }
 
-// Coarse histogram of the whole row into sm.hist (clear before a preceding
-// barrier); ends with a barrier.
-__device__ __forceinline__ void exact_hist(const KArgs a, Smem &sm, int64_t off, int64_t L) {
-    stream_row<false>(a.scores, off, 0, (int32_t)L,
+// Coarse histogram of row elements [beg, end) into sm.hist (clear before a
+// preceding barrier); ends with a barrier.
+__device__ __forceinline__ void exact_hist(const KArgs a, Smem &sm, int64_t off, int32_t beg,
+                                           int32_t end) {
+    stream_row<false>(a.scores, off, beg, end,
                       [&](const f4 *x, const int32_t *i0, int32_t lo, int32_t hi, bool edge,
                           int32_t mv) { coarse_hist_chunk(sm, x, i0, lo, hi, edge, mv); });
     __syncthreads();
@@ -1377,6 +1401,29 @@ __device__ __forceinline__ int64_t view_size(int64_t L, uint32_t a, int s_log2) 
 // half an FP64 ulp of n + 1, so the rounded quotient stays below n + 1.
 __device__ __forceinline__ uint32_t udiv32(uint32_t x, uint32_t y) {
     return (uint32_t)floor((double)x / (double)y);
+}
+
+// Whether row r is sampled (Section 4.2: long enough for the floor and its
+// view at least q1 samples); rows of length <= K take the direct route.
+__device__ __forceinline__ bool row_sampled(const KArgs &a, int r, int64_t L) {
+    return L > a.K && L >= a.l_samp_min &&
+           view_size(L, view_phase(r, a.s_log2), a.s_log2) >= a.q1;
+}
+
+// Segment length of a row that the item table cuts into Pe pieces: a multiple
+// of 64 elements giving exactly Pe of them (Pe - 1 pieces of 64 ceil(L / 64 Pe)
+// < L / Pe + 64 elements fall short of L, as L / Pe >= kSegMin > 64 Pe).
+__device__ __forceinline__ int64_t table_seg(int64_t L, int Pe) {
+    return 64 * (int64_t)udiv32((uint32_t)L + 64u * (uint32_t)Pe - 1u, 64u * (uint32_t)Pe);
+}
+
+// Entry of the item table: row | segment << 14 | (segments - 1) << 20 in x
+// (bit 31: no work), the length in y, the offset's low 32 bits in z, its bits
+// 32..39 and the row-state slot << 8 in w.
+__device__ __forceinline__ uint4 order_entry(uint32_t r, uint32_t p, uint32_t P, int32_t L,
+                                             uint64_t o, uint32_t slot) {
+    return make_uint4(r | (p << 14) | ((P - 1u) << 20), (uint32_t)L, (uint32_t)o,
+                      ((uint32_t)(o >> 32) & 0xFFu) | (slot << 8));
 }
 
 // Sum of max(L_r, 0) over all rows of the call (every workgroup of a
@@ -1878,15 +1925,312 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
 // ----------------------------------------------------------- kernel ----
 
 // Leaves a split row's state zeroed for the next call (graph replays).
-__device__ __forceinline__ void reset_row_state(RowState *rs) {
+// x: also the split exact route's fields (written only in calls run from
+// the item table).
+__device__ __forceinline__ void reset_row_state(RowState *rs, bool x = true) {
     __hip_atomic_store(&rs->counts, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->sa, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->incomplete, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->amax, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->varrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!x) return;
+    __hip_atomic_store(&rs->xtau, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->ocnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->qcnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->arrive2, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->xbelow, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->xeq, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->xmask, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ------------------------------------------- split exact recovery ----
+//
+// Exact coarse recovery (eq:method:exact-init) of a split row whose
+// candidates overflowed, spread over its segments.  Every segment with an
+// overflowed region has added the coarse histogram of its range into the
+// row's histogram; the finisher adds the other segments' stored candidates
+// (all of their elements with c <= tau1), which makes the histogram exact in
+// bins 0..tau1, where tau_star lies when C(tau1) >= K.  It publishes
+// tau_star, and each segment then classifies its own range (the finisher the
+// stored candidates): c < tau_star into the row's output (E0), c == tau_star
+// into the candidate buffer (Q0), at slots reserved with one atomic per
+// segment from its own histogram's counts.  The last to finish refines Q0.
+
+constexpr uint32_t kXGo = 0x80000000u, kXAbandon = 0x40000000u;
+
+// Entries of h in bins < t and in bin t, into sm.cnt0 and sm.cnt (zero
+// before a preceding barrier).  Ends with a barrier.
+__device__ __forceinline__ void hist_lt_eq(Smem &sm, const uint32_t *h, uint32_t t) {
+    const uint32_t t4 = 4u * (uint32_t)threadIdx.x;
+    const uint4 v = reinterpret_cast<const uint4 *>(h)[threadIdx.x];
+    const uint32_t lt = (t4 < t ? v.x : 0u) + (t4 + 1u < t ? v.y : 0u) +
+                        (t4 + 2u < t ? v.z : 0u) + (t4 + 3u < t ? v.w : 0u);
+    const uint32_t eq = (t4 == t ? v.x : 0u) + (t4 + 1u == t ? v.y : 0u) +
+                        (t4 + 2u == t ? v.z : 0u) + (t4 + 3u == t ? v.w : 0u);
+    const uint32_t clt = wave_incl_scan(lt), ceq = wave_incl_scan(eq);
+    if ((threadIdx.x & 63) == 63) {
+        if (clt) atomicAdd(&sm.cnt0, clt);
+        if (ceq) atomicAdd(&sm.cnt, ceq);
+    }
+    __syncthreads();
+}
+
+// Classify pass over row elements [beg, end): ascending keys u >= key_hi
+// (c < tau_star) go to the row's output at glt + rank, key_lo <= u < key_hi
+// (c == tau_star) to gc[geq + rank] as index | FP32 bits << 32; the caller
+// reserved [glt, glt + n_lt) and [geq, geq + n_eq), the range's counts of the
+// two.  Appends are wave-aggregated per chunk (bit masks, one wave scan, one
+// LDS atomic per category); when both sets fit the LDS pairs they are staged
+// there and written out after the pass, so that the loop stores nothing to
+// global memory.  sm.opos and sm.cnt must be zero before a preceding
+// barrier.  Ends with a barrier.
+__device__ __forceinline__ void classify_range(const KArgs a, Smem &sm, int r, int64_t off,
+                                            int32_t beg, int32_t end, uint32_t key_lo,
+                                            uint32_t key_hi, uint32_t n_lt, uint32_t n_eq,
+                                            uint32_t glt, uint32_t geq, uint64_t *gc) {
+    const int tid = threadIdx.x;
+    const int lane = lane_id();
+    const bool stage = n_lt + n_eq <= (uint32_t)kFront;
+    const uint32_t top = (uint32_t)kFront - n_lt; // staged E0 at [top, kFront)
+    int32_t *oi = a.out_idx + (int64_t)r * a.K;
+    float *ov = a.out_val + (int64_t)r * a.K;
+    static_assert(kVec * 4 <= 16 && kWaves * 64 * 16 < 65536, "packed counts");
+    stream_row<false>(a.scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                                   int32_t hi, bool edge, int32_t mv) {
+        uint32_t mlt = 0, meq = 0;
+#pragma unroll
+        for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+                const uint32_t u = asc_key(fbits(x[m][c]));
+                const bool in = !edge || in_window(i0[m] + c, lo, hi);
+                mlt |= (in && u >= key_hi ? 1u : 0u) << (m * 4 + c);
+                meq |= (in && u >= key_lo && u < key_hi ? 1u : 0u) << (m * 4 + c);
+            }
+        }
+        const uint32_t packed = (uint32_t)__popc(mlt) | ((uint32_t)__popc(meq) << 16);
+        const uint32_t incl = wave_incl_scan(packed);
+        const uint32_t tot = __builtin_amdgcn_readlane(incl, 63);
+        if (tot == 0) return;
+        uint32_t bl = 0, be = 0;
+        if (lane == 0) {
+            if (tot & 0xFFFFu) bl = atomicAdd(&sm.opos, tot & 0xFFFFu);
+            if (tot >> 16) be = atomicAdd(&sm.cnt, tot >> 16);
+        }
+        const uint32_t excl = incl - packed;
+        uint32_t pl = __builtin_amdgcn_readfirstlane(bl) + (excl & 0xFFFFu);
+        uint32_t pe = __builtin_amdgcn_readfirstlane(be) + (excl >> 16);
+#pragma unroll
+        for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+                const int b = m * 4 + c;
+                const uint32_t i = (uint32_t)(i0[m] + c);
+                const uint32_t bits = fbits(x[m][c]);
+                if ((mlt >> b) & 1u) {
+                    // (never false for consistent counts)
+                    if (pl < n_lt && glt + pl < (uint32_t)a.K) {
+                        if (stage) {
+                            sm.ci[top + pl] = i;
+                            sm.ck[top + pl] = bits;
+                        } else {
+                            oi[glt + pl] = (int32_t)i;
+                            ov[glt + pl] = x[m][c];
+                        }
+                    }
+                    pl++;
+                }
+                if ((meq >> b) & 1u) {
+                    if (pe < n_eq && geq + pe < (uint32_t)kFront) {
+                        if (stage) {
+                            sm.ci[pe] = i;
+                            sm.ck[pe] = bits;
+                        } else {
+                            __hip_atomic_store(&gc[geq + pe], (uint64_t)i | ((uint64_t)bits << 32),
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                    }
+                    pe++;
+                }
+            }
+        }
+    });
+    if (stage) {
+        __syncthreads();
+        for (uint32_t e = (uint32_t)tid; e < n_lt && glt + e < (uint32_t)a.K; e += kBlock) {
+            oi[glt + e] = (int32_t)sm.ci[top + e];
+            ov[glt + e] = __builtin_bit_cast(float, sm.ck[top + e]);
+        }
+        for (uint32_t e = (uint32_t)tid; e < n_eq && geq + e < (uint32_t)kFront; e += kBlock)
+            __hip_atomic_store(&gc[geq + e], (uint64_t)sm.ci[e] | ((uint64_t)sm.ck[e] << 32),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+}
+
+// Counts of the histogram h (LDS) for tau_star, the reservation of their
+// slots, and the classify pass over [beg, end).  Ends with a barrier.
+__device__ __forceinline__ void classify_own_range(const KArgs a, Smem &sm, int r, int64_t off,
+                                                   int32_t beg, int32_t end, const uint32_t *h,
+                                                   uint32_t ts, RowState *rs, uint64_t *gc) {
+    if (threadIdx.x == 0) { sm.cnt0 = 0; sm.cnt = 0; sm.opos = 0; }
+    __syncthreads();
+    hist_lt_eq(sm, h, ts);
+    const uint32_t n_lt = sm.cnt0, n_eq = sm.cnt;
+    __syncthreads(); // every thread has read the counts
+    if (threadIdx.x == 0) {
+        sm.cnt = 0;
+        sm.flag = n_lt ? __hip_atomic_fetch_add(&rs->ocnt, n_lt, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT) : 0u;
+        sm.base = n_eq ? __hip_atomic_fetch_add(&rs->qcnt, n_eq, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT) : 0u;
+    }
+    __syncthreads();
+    const uint32_t glt = sm.flag, geq = sm.base;
+    const uint32_t key_hi = ts > 0 ? bin_cutoff(ts - 1u) : 0xFFFFFFFFu, key_lo = bin_cutoff(ts);
+    classify_range(a, sm, r, off, beg, end, key_lo, key_hi, n_lt, n_eq, glt, geq, gc);
+}
+
+// The finisher's share: the complete segments' stored candidates, held in
+// registers (slot j kBlock + tid < stored).  Ends with a barrier.
+__device__ __forceinline__ void classify_stored(const KArgs a, Smem &sm, int r, RowState *rs,
+                                                uint64_t *gc, const uint32_t (&vi)[kPer],
+                                                const uint32_t (&vk)[kPer], uint32_t stored,
+                                                uint32_t ts) {
+    const int tid = threadIdx.x;
+    const uint32_t w8 = (uint32_t)tid >> 6;
+    const uint32_t key_hi = ts > 0 ? bin_cutoff(ts - 1u) : 0xFFFFFFFFu, key_lo = bin_cutoff(ts);
+    uint32_t nl = 0, ne = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const uint32_t u = asc_key(vk[j]);
+        const bool in = (uint32_t)(j * kBlock + tid) < stored;
+        nl += (in && u >= key_hi) ? 1u : 0u;
+        ne += (in && u >= key_lo && u < key_hi) ? 1u : 0u;
+    }
+    // per-thread counts of at most kPer, wave sums below 2^16
+    const uint32_t own = nl | (ne << 16);
+    const uint32_t incl = wave_incl_scan(own);
+    if (lane_id() == 63) sm.wc[w8] = incl;
+    __syncthreads();
+    uint32_t wpre = 0, tot = 0;
+#pragma unroll
+    for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
+        const uint32_t c = sm.wc[v];
+        wpre += v < w8 ? c : 0u;
+        tot += c;
+    }
+    if (tid == 0) {
+        sm.flag = (tot & 0xFFFFu) ? __hip_atomic_fetch_add(&rs->ocnt, tot & 0xFFFFu, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT) : 0u;
+        sm.base = (tot >> 16) ? __hip_atomic_fetch_add(&rs->qcnt, tot >> 16, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT) : 0u;
+    }
+    __syncthreads();
+    const uint32_t first = wpre + incl - own;
+    uint32_t pl = sm.flag + (first & 0xFFFFu), pe = sm.base + (first >> 16);
+    int32_t *oi = a.out_idx + (int64_t)r * a.K;
+    float *ov = a.out_val + (int64_t)r * a.K;
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const uint32_t u = asc_key(vk[j]);
+        const bool in = (uint32_t)(j * kBlock + tid) < stored;
+        if (in && u >= key_hi) {
+            if (pl < (uint32_t)a.K) { // never false for consistent counts
+                oi[pl] = (int32_t)vi[j];
+                ov[pl] = __builtin_bit_cast(float, vk[j]);
+            }
+            pl++;
+        } else if (in && u >= key_lo) {
+            if (pe < (uint32_t)kFront)
+                __hip_atomic_store(&gc[pe], (uint64_t)vi[j] | ((uint64_t)vk[j] << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            pe++;
+        }
+    }
+    __syncthreads();
+}
+
+// Second arrival at a split row in the exact route; xt0 is the arriving
+// segment's view of the route word (0: it stopped waiting, and its segment
+// bit in xmask is set first).  Returns the route word for the last arrival,
+// 0 for the others.  Each wave's stores complete before the barrier that
+// precedes the arrival (as for the first arrival).
+__device__ __forceinline__ uint32_t arrive_again(Smem &sm, RowState *rs, int p, uint32_t xt0) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (!(xt0 & kXGo)) {
+            __hip_atomic_fetch_or(&rs->xmask, 1ull << p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0); // the bit is set before the arrival counts
+        }
+        const uint32_t old = __hip_atomic_fetch_add(&rs->arrive2, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        // the finisher publishes the route word before its own arrival, so a
+        // last arrival always sees it
+        const uint32_t xt = __hip_atomic_load(&rs->xtau, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.flag = ((xt & kXGo) && old + 1u == ((xt >> 11) & 0xFFu)) ? xt : 0u;
+    }
+    __syncthreads();
+    return sm.flag;
+}
+
+// The last arrival of the split exact route: loads Q0 and refines it for the
+// remaining K - |E0| outputs, records the row and resets its state.  Returns
+// false, with nothing done, when a segment stopped waiting (its range is not
+// classified): the caller then runs the whole row's exact route, which
+// rewrites every output; sm.wk[2] and sm.wk[3] hold C(tau1) and C(tau0).
+__device__ __forceinline__ bool split_exact_final(const KArgs a, Smem &sm, int r, int64_t nv,
+                                                  RowState *rs, uint64_t *gc, uint32_t xt) {
+    const int tid = threadIdx.x;
+    const uint32_t ts = xt & 0x7FFu;
+    if (tid == 0) {
+        sm.wc[0] = __hip_atomic_load(&rs->xbelow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.wc[1] = __hip_atomic_load(&rs->xeq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t m = __hip_atomic_load(&rs->xmask, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.wk[0] = (uint32_t)m;
+        sm.wk[1] = (uint32_t)(m >> 32);
+        const uint64_t cc = __hip_atomic_load(&rs->counts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.wk[2] = (uint32_t)cc;
+        sm.wk[3] = (uint32_t)(cc >> 32);
+    }
+    __syncthreads();
+    const uint32_t below = sm.wc[0], eq = sm.wc[1];
+    if (sm.wk[0] | sm.wk[1]) return false;
+    const uint32_t C1 = sm.wk[2], C0 = sm.wk[3];
+    // Q0: the kept entries, as kappa32 keys
+    for (uint32_t e = (uint32_t)tid; e < min(eq, (uint32_t)kFront); e += kBlock) {
+        const uint64_t v = __hip_atomic_load(&gc[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.ci[e] = (uint32_t)v;
+        sm.ck[e] = ~asc_key((uint32_t)(v >> 32));
+    }
+    clear_hist(sm);
+    reset_range(sm);
+    if (tid == 0) sm.opos = 0;
+    __syncthreads();
+    const uint32_t amin = bin_cutoff(ts);
+    const uint32_t amax = ts > 0 ? bin_cutoff(ts - 1u) - 1u : 0xFFFFFFFFu;
+    refine(a, sm, r, false, eq, false, amin, amax >= amin ? amax : 0u, eq, (uint32_t)a.K - below);
+    PHASE_MARK(a, 13);
+    if (tid == 0) {
+        atomicAdd(&a.hdr->stats[TOPK_ROUTE_EXACT_OVERFLOW], 1u);
+        if (a.trace) {
+            int32_t *t = a.trace + (int64_t)r * TOPK_TRACE_WORDS;
+            t[0] = TOPK_ROUTE_EXACT_OVERFLOW; t[1] = (int32_t)nv;
+            t[2] = (int32_t)sm.tau0; t[3] = (int32_t)sm.tau1;
+            t[4] = (int32_t)C0; t[5] = C0 < (uint32_t)a.K ? (int32_t)C1 : -1;
+            t[6] = (int32_t)ts; t[7] = (int32_t)eq;
+        }
+        reset_row_state(rs);
+    }
+    return true;
+}
+
+// kOrdered: the call runs from the item table (a.order set).  Only such calls
+// take the split exact route; the other instance has none of its code (with
+// it, the decode batch measured 3 % slower although it never runs it).
+template <bool kOrdered>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void
 topk_ragged_kernel(KArgs a) {
     __shared__ Smem sm;
@@ -1897,15 +2241,14 @@ topk_ragged_kernel(KArgs a) {
         for (int k = 0; k < 32; k++) g_tmarks[k] = 0;
     TimerFlush timer_flush{a.timers};
 #endif
-    const int p = item / a.n_rows;
+    const int pi = item / a.n_rows;
     // Every load the prologue needs goes out at once: the row's length and
-    // offset (from the longest-first order when the call has one, p = 0
-    // then), the workspace header, and this thread's first term of the
-    // segment plan's length sum (used only when rows may be split).
-    // (all loaded unconditionally and selected afterwards: a branch here
-    // would cost a second round trip; with an order, p = 0 and item < n_rows)
-    const bool ordered = a.order != nullptr;
-    const int ri = item - p * a.n_rows;
+    // offset (from the item table when the call has one), the workspace
+    // header, and this thread's first term of the segment plan's length sum
+    // (used only when rows may be split).  (all loaded unconditionally and
+    // selected afterwards: a branch here would cost a second round trip)
+    constexpr bool ordered = kOrdered;
+    const int ri = item - pi * a.n_rows;
     const uint4 e = *(ordered ? a.order + item : reinterpret_cast<const uint4 *>(a.hdr));
     const int32_t len_i = a.lens[ri];
     const int64_t off_i = a.offs[ri];
@@ -1915,9 +2258,15 @@ topk_ragged_kernel(KArgs a) {
     // would make them several round trips instead of one)
     asm volatile("" ::"s"(e.x), "s"(e.y), "s"(e.z), "s"(e.w), "s"(len_i), "s"(off_i), "s"(hw.x),
                  "s"(hw.y), "s"(hw.z), "v"(len0_raw));
-    const int r = ordered ? (int)e.x : ri;
+    if (ordered && (e.x >> 31)) return; // an item past the call's last segment
+    // the row, its segment, the segments the item table gives it (0: none,
+    // the plan decides), and its row-state block
+    const int r = ordered ? (int)(e.x & 0x3FFFu) : ri;
+    const int p = ordered ? (int)((e.x >> 14) & 63u) : pi;
+    const int Pe = ordered ? (int)((e.x >> 20) & 63u) + 1 : 0;
+    const uint32_t slot = ordered ? e.w >> 8 : (uint32_t)r;
     const int32_t len_r = ordered ? (int32_t)e.y : len_i;
-    const int64_t off = ordered ? (int64_t)(((uint64_t)e.w << 32) | e.z) : off_i;
+    const int64_t off = ordered ? (int64_t)((((uint64_t)e.w & 0xFFu) << 32) | e.z) : off_i;
     const int64_t L = (int64_t)max(len_r, 0);
     const float *row = a.scores + off;
     PHASE_MARK(a, 0);
@@ -1960,17 +2309,22 @@ topk_ragged_kernel(KArgs a) {
 
     const uint32_t ph = view_phase(r, a.s_log2);
     const int64_t nv = view_size(L, ph, a.s_log2);
-    const bool sampled = L >= a.l_samp_min && nv >= a.q1;
+    const bool sampled = row_sampled(a, r, L);
     if (!sampled && p > 0) return; // unsampled rows run whole on segment 0
 
-    RowState *rs = reinterpret_cast<RowState *>(a.rows + (size_t)r * kRowBlockBytes);
+    char *rb = a.rows + (size_t)slot * kRowBlockBytes;
+    RowState *rs = reinterpret_cast<RowState *>(rb);
+    uint32_t *vh = reinterpret_cast<uint32_t *>(rb + kRowStateBytes);
+    uint32_t *xh = reinterpret_cast<uint32_t *>(a.rows + (size_t)hw.y * kRowBlockBytes) +
+                   (size_t)slot * kBins;
     // the row's merged candidates: index | FP32 bits << 32
-    uint32_t *vh = reinterpret_cast<uint32_t *>(a.rows + (size_t)r * kRowBlockBytes +
-                                                kRowStateBytes);
-    uint64_t *gc = reinterpret_cast<uint64_t *>(a.rows + (size_t)r * kRowBlockBytes +
-                                                kRowStateBytes + kViewHistBytes);
+    uint64_t *gc = reinterpret_cast<uint64_t *>(rb + kRowStateBytes + kViewHistBytes);
     uint32_t C0 = 0, C1 = 0, nstored = 0;
     bool incomplete = false, segmented = true, split = false, have_hist = false;
+    // split exact route: this segment added its coarse histogram; second
+    // arrivals the finisher expects (0: none)
+    bool pushed = false, redo = false;
+    uint32_t xexpect = 0;
 
     if (sampled) {
         // A row has at most ceil(L / kSegMin) segments (see below).
@@ -1982,12 +2336,17 @@ topk_ragged_kernel(KArgs a) {
         // chunk in flight.  A large view of a split row is shared instead:
         // each segment reads the part inside its own range (after the plan).
         float xs[kP1];
-        const bool big_view = nv >= kCoopView && a.pmax > 1;
+        const bool big_view = nv >= kCoopView && (a.pmax > 1 || Pe > 1);
         if (p == 0 && !big_view) phase1_issue(a, r, row, L, xs);
-        // Segments (segment_plan) when rows may be split.
+        // Segments: segment_plan when every row may be split, else the item
+        // table's count.
         int64_t P = 1, seg = L;
-        if (a.pmax > 1)
+        if (a.pmax > 1) {
             segment_plan(a, block_total_length(a, sm.lsum, tid < a.n_rows ? len0_raw : 0), L, P, seg);
+        } else if (Pe > 1) {
+            P = Pe;
+            seg = table_seg(L, Pe);
+        }
         if (p >= P) return;
         split = P > 1;
         const int32_t beg = (int32_t)(p * seg);
@@ -2064,11 +2423,13 @@ topk_ragged_kernel(KArgs a) {
         // C(tau0)), adds its two counts in one 64-bit atomic and its maximum,
         // and copies its region; a wave whose region overflowed re-counts the
         // positions it streams and marks the row incomplete.  With many
-        // segments (whose per-wave atomics on the same words would queue) the
-        // workgroup counts and publishes as one.  Either way the workgroup
+        // segments (whose per-wave atomics on the same words would queue), and
+        // in a call run from the item table, the workgroup counts and
+        // publishes as one, and a segment with an overflowed region publishes
+        // its coarse histogram instead of entries.  Either way the workgroup
         // arrives once.
         const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
-        const bool wave_publish = split && P <= kWavePublishMaxSegs;
+        const bool wave_publish = split && P <= kWavePublishMaxSegs && !ordered;
         uint32_t wcnt = 0, dst = 0; // this wave's stored entries, and their first slot
         if (wave_publish) {
             const uint32_t cur_w = sm.wcnt[w8]; // this wave's own count
@@ -2112,9 +2473,10 @@ topk_ragged_kernel(KArgs a) {
             incomplete = sm.incomplete != 0;
             uint32_t wpre = 0, nst = 0, resv = 0;
             if (split) {
+                // (an incomplete segment publishes a histogram instead)
 #pragma unroll
                 for (uint32_t v = 0; v < (uint32_t)kWaves; v++) {
-                    const uint32_t cv = min(sm.wcnt[v], (uint32_t)kWaveCap);
+                    const uint32_t cv = incomplete ? 0u : min(sm.wcnt[v], (uint32_t)kWaveCap);
                     wcnt = v == w8 ? cv : wcnt;
                     wpre += v < w8 ? cv : 0u;
                     nst += cv;
@@ -2125,22 +2487,32 @@ topk_ragged_kernel(KArgs a) {
                                                             __HIP_MEMORY_SCOPE_AGENT);
             }
             // C(tau0): from the stored A(tau1) entries.  When a wave region
-            // overflowed (that wave stopped early), C(tau0) and C(tau1) are
-            // counted by re-reading this segment; a row on one workgroup
-            // re-reads it for the coarse histogram instead, which gives both
-            // counts and is the first pass of the exact route, should the row
-            // take it.
+            // overflowed (that wave stopped early), this segment is re-read
+            // for its coarse histogram, which gives C(tau0) and C(tau1) and is
+            // the first pass of the exact route, should the row take it: a
+            // row on one workgroup keeps it, a split row's segment adds it
+            // into the row's coarse histogram xh for the finisher.
             if (__builtin_expect(incomplete, 0)) {
                 __syncthreads(); // every thread has read sm.cnt
                 if (tid == 0) sm.cnt = 0; // (sm.cnt0 is still zero)
-                if (!split) clear_hist(sm);
+                if (!split || kOrdered) clear_hist(sm);
                 __syncthreads();
-                if (!split) {
-                    exact_hist(a, sm, off, L);
-                    hist_counts(sm, sm.tau0, sm.tau1);
-                    have_hist = true;
-                } else {
+                if (split && !kOrdered) {
                     count_range(sm, a.scores, off, beg, end, sm.cut0, sm.cut1);
+                } else {
+                    exact_hist(a, sm, off, beg, end);
+                    hist_counts(sm, sm.tau0, sm.tau1);
+                }
+                if (!split) {
+                    have_hist = true;
+                } else if (kOrdered) {
+                    const uint4 h = reinterpret_cast<const uint4 *>(sm.hist)[tid];
+                    uint32_t *d = xh + 4 * tid;
+                    if (h.x) __hip_atomic_fetch_add(d + 0, h.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (h.y) __hip_atomic_fetch_add(d + 1, h.y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (h.z) __hip_atomic_fetch_add(d + 2, h.z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (h.w) __hip_atomic_fetch_add(d + 3, h.w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    pushed = true; // (and sm.hist is kept for the classify pass)
                 }
                 C0 = sm.cnt0;
                 C1 = sm.cnt;
@@ -2155,8 +2527,8 @@ topk_ragged_kernel(KArgs a) {
                         __hip_atomic_fetch_add(&rs->counts, (uint64_t)C1 | ((uint64_t)C0 << 32),
                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     if (incomplete)
-                        __hip_atomic_store(&rs->incomplete, 1u, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_fetch_add(&rs->incomplete, 1u, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
                     else if (nst)
                         __hip_atomic_fetch_max(&rs->amax, sm.amax, __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
@@ -2178,7 +2550,7 @@ topk_ragged_kernel(KArgs a) {
             }
             // (the histogram is cleared for the finisher's use while the
             // copies complete)
-            clear_hist(sm);
+            if (!pushed) clear_hist(sm);
             // Every value another workgroup reads (entries, counts, the
             // arrival counter) is an agent-scope atomic access, which the
             // hardware keeps coherent across the XCDs' L2 caches without a
@@ -2195,8 +2567,40 @@ topk_ragged_kernel(KArgs a) {
             }
             __syncthreads();
             PHASE_MARK(a, 3);
-            if (sm.flag != 2u) return;
+            if (sm.flag != 2u) {
+                if (__builtin_expect(!pushed, 1)) return;
+                // Split exact route: wait for the finisher's route word
+                // (bounded as the boundary wait; after it the last arrival
+                // classifies this range), classify this range, arrive again.
+                if (tid == 0) {
+                    uint32_t v = 0;
+                    const uint64_t t_wait = wall_clock64();
+                    for (int spin = 0; spin < a.spin_limit; spin++) {
+                        v = __hip_atomic_load(&rs->xtau, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if ((v & kXGo) || wall_clock64() - t_wait > a.spin_ticks) break;
+                        __builtin_amdgcn_s_sleep(1);
+                    }
+                    sm.xword = v;
+                    if (!(v & kXGo)) atomicAdd(&a.hdr->stats[kStatWaitFallback], 1u);
+                }
+                __syncthreads();
+                const uint32_t xv = sm.xword;
+                if ((xv & (kXGo | kXAbandon)) == kXGo)
+                    classify_own_range(a, sm, r, off, beg, end, sm.hist, xv & 0x7FFu, rs, gc);
+                const uint32_t xt = arrive_again(sm, rs, p, xv);
+                if (!xt) return;
+                if (xt & kXAbandon) {
+                    if (tid == 0) reset_row_state(rs);
+                    return;
+                }
+                if (split_exact_final(a, sm, r, nv, rs, gc, xt)) {
+                    PHASE_MARK(a, 5);
+                    return;
+                }
+                redo = true;
+            }
 
+            if (!redo) {
             // Finisher (its sm.cut0, cut1, tau0, tau1 are the row's endpoints).
             // The counts and the slot groups that hold candidates are loaded
             // in one round trip (slots past the stored count in the last
@@ -2235,7 +2639,7 @@ topk_ragged_kernel(KArgs a) {
                 finish_fast(a, sm, r, nv, C0, C1, amx, kBlock, (uint32_t)tid, nstored,
                             ngroups, vi, vk)) {
                 PHASE_MARK(a, 5);
-                if (tid == 0) reset_row_state(rs);
+                if (tid == 0) reset_row_state(rs, false); // (no segment took the exact route)
                 return;
             }
             // general finish: the merged frontier into LDS
@@ -2248,7 +2652,84 @@ topk_ragged_kernel(KArgs a) {
                     sm.ck[t] = vk[j];
                 }
             }
+            // segments that added a coarse histogram (block publishing only)
+            const uint32_t nx =
+                kOrdered && !wave_publish ? __builtin_amdgcn_readfirstlane(inc) : 0u;
+            if (__builtin_expect(nx != 0, 0)) {
+                // The overflowed segments' merged coarse histogram, cleared
+                // for the next call once read (this segment's own, if it
+                // added one, is kept in sm.ck for its classify pass).  Every
+                // other segment stored all of its elements with c <= tau1;
+                // with them added the histogram is the row's own in bins
+                // 0..tau1, which holds tau_star whenever C(tau1) >= K (an
+                // overflowing row).
+                uint64_t *d = reinterpret_cast<uint64_t *>(xh + 4 * tid);
+                const uint64_t lo = __hip_atomic_load(d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint64_t hi = __hip_atomic_load(d + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (pushed)
+                    reinterpret_cast<uint4 *>(sm.ck)[tid] = reinterpret_cast<const uint4 *>(sm.hist)[tid];
+                reinterpret_cast<uint4 *>(sm.hist)[tid] =
+                    make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32));
+                __hip_atomic_store(d, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(d + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t cap = (uint32_t)a.cap, K = (uint32_t)a.K;
+                have_hist = stored <= (uint32_t)kFront && (C0 > cap || (C0 < K && C1 > cap));
+                if (have_hist) {
+                    __syncthreads();
+#pragma unroll
+                    for (int j = 0; j < kPer; j++)
+                        if ((uint32_t)(j * kBlock + tid) < stored)
+                            atomicAdd(&sm.hist[coarse_bin(__builtin_bit_cast(float, vk[j]))], 1u);
+                }
+                __syncthreads();
+                bool dist = false;
+                if (have_hist) {
+                    if (tid < 64) wave_find(sm.hist, K, 0, 1, sm.find);
+                    __syncthreads();
+                    dist = sm.find[0].eq <= cap;
+                }
+                // every segment that added a histogram waits for the route
+                // word; this workgroup arrives once more as well
+                xexpect = nx + (pushed ? 0u : 1u);
+                if (dist) {
+                    const Find f = sm.find[0];
+                    if (tid == 0) {
+                        __hip_atomic_store(&rs->xbelow, f.below, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&rs->xeq, f.eq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&rs->xtau, kXGo | (xexpect << 11) | f.bin, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    PHASE_MARK(a, 4);
+                    classify_stored(a, sm, r, rs, gc, vi, vk, stored, f.bin);
+                    if (pushed) classify_own_range(a, sm, r, off, beg, end, sm.ck, f.bin, rs, gc);
+                    const uint32_t xt = arrive_again(sm, rs, p, kXGo);
+                    if (!xt) return;
+                    if (split_exact_final(a, sm, r, nv, rs, gc, xt)) {
+                        PHASE_MARK(a, 5);
+                        return;
+                    }
+                    redo = true;
+                } else if (tid == 0) {
+                    // any other route runs here, on this workgroup
+                    __hip_atomic_store(&rs->xtau, kXGo | kXAbandon | (xexpect << 11), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
             __syncthreads();
+            } // !redo
+            if (__builtin_expect(redo, 0)) {
+                // A segment of the split exact route stopped waiting: this
+                // last arrival runs the row's exact route on its own, which
+                // rewrites every output (the others are done with the row).
+                C1 = sm.wk[2];
+                C0 = sm.wk[3];
+                incomplete = true;
+                nstored = 0;
+                segmented = false;
+                have_hist = false;
+                xexpect = 0;
+                __syncthreads();
+            }
         }
     }
 
@@ -2283,7 +2764,14 @@ topk_ragged_kernel(KArgs a) {
     finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored, have_hist);
     PHASE_MARK(a, 5);
 
-    if (split && tid == 0) reset_row_state(rs);
+    // the row state is reset once every segment is done with it
+    if (split) {
+        if (xexpect) {
+            if (arrive_again(sm, rs, p, kXGo) && tid == 0) reset_row_state(rs);
+        } else if (tid == 0) {
+            reset_row_state(rs, kOrdered && redo);
+        }
+    }
 }
 
 // Length class of a row for the longest-first order: 8 classes per octave
@@ -2295,29 +2783,49 @@ __device__ __forceinline__ uint32_t length_class(int32_t L) {
     return e * 8u + (((uint32_t)L >> (e - 3u)) & 7u);
 }
 
-// Pre-pass of a call whose rows each take one workgroup: a counting sort of
-// the rows by length class, longest first (any order within a class), into
-// order[0, n) as (row, length, offset low, offset high).  One workgroup;
-// n <= kOrderMaxRows.  Thread t takes rows [kOrderPer t, kOrderPer (t + 1)),
-// and a run of equal classes among them takes one LDS atomic: rows of
-// similar length would otherwise all add into one counter at once.
-__global__ __launch_bounds__(kOrderBlock) void row_order_kernel(const int64_t *offs,
-                                                                const int32_t *lens, int32_t n,
-                                                                uint4 *order) {
+// Pre-pass of a call with more rows than resident workgroups: a counting
+// sort of the rows by length class, longest first (any order within a
+// class), then the work items in that order into order[0, n + extra).
+// One workgroup; n <= kOrderMaxRows, extra <= kOrderExtra.  Thread t takes
+// rows [kOrderPer t, kOrderPer (t + 1)), and a run of equal classes among
+// them takes one LDS atomic: rows of similar length would otherwise all add
+// into one counter at once.
+//
+// Splitting (KV-split mapping, Section 4.5, for calls too large to split
+// every row): a sampled row among the kOrderBlock longest gets
+// P = min(kMaxSplit, L / kSegMin, ceil(L / S)) segments, S = max(kSegMin,
+// sum(L) / slots), the mean work of a resident workgroup, so that no row
+// outlasts the call on one workgroup.  Going down the order, rows keep their
+// segments while the extra items stay within `extra` and the split rows
+// within the workspace's per-row state (slot k for the k-th split row);
+// every later row runs whole.  A row's segments are consecutive items, and
+// items past the last are marked empty.
+__global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *order,
+                                                                int32_t extra, int32_t slots) {
     constexpr uint32_t kNone = 256; // class of a position past the last row
+    constexpr int kW = kOrderBlock / 64;
     __shared__ uint32_t cnt[256];
+    __shared__ uint32_t rinfo[kOrderBlock]; // by rank: extra segments, then the plan
+    __shared__ uint32_t wtot[kW];
+    __shared__ int64_t lsum[kW];
+    __shared__ uint32_t ecap_s;
+    const int n = a.n_rows;
     const int tid = threadIdx.x;
+    const int w = tid >> 6;
     const int i0 = tid * kOrderPer;
     if (tid < 256) cnt[tid] = 0;
+    if (tid == 0) ecap_s = 0;
+    rinfo[tid] = 0;
+    const uint32_t max_split = a.hdr->split_rows;
     int32_t Ls[kOrderPer];
     int64_t Os[kOrderPer]; // loaded with the lengths: one round trip to memory
     // (16-byte loads where the arrays allow: each thread's rows are
     // contiguous, so the lanes of one load are 64 bytes apart)
-    const bool vec = ((reinterpret_cast<uintptr_t>(lens) | reinterpret_cast<uintptr_t>(offs)) &
-                      15u) == 0 && i0 + kOrderPer <= n;
+    const bool vec = ((reinterpret_cast<uintptr_t>(a.lens) |
+                       reinterpret_cast<uintptr_t>(a.offs)) & 15u) == 0 && i0 + kOrderPer <= n;
     if (vec) {
-        const int4 *l4 = reinterpret_cast<const int4 *>(lens + i0);
-        const longlong2 *o2 = reinterpret_cast<const longlong2 *>(offs + i0);
+        const int4 *l4 = reinterpret_cast<const int4 *>(a.lens + i0);
+        const longlong2 *o2 = reinterpret_cast<const longlong2 *>(a.offs + i0);
 #pragma unroll
         for (int q = 0; q < kOrderPer / 4; q++) {
             const int4 v = l4[q];
@@ -2331,8 +2839,8 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(const int64_t *o
     } else {
 #pragma unroll
         for (int j = 0; j < kOrderPer; j++) {
-            Ls[j] = i0 + j < n ? lens[i0 + j] : 0;
-            Os[j] = i0 + j < n ? offs[i0 + j] : 0;
+            Ls[j] = i0 + j < n ? a.lens[i0 + j] : 0;
+            Os[j] = i0 + j < n ? a.offs[i0 + j] : 0;
         }
     }
     uint32_t cls[kOrderPer], run[kOrderPer]; // run[j]: rows of j's run from j on
@@ -2341,6 +2849,17 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(const int64_t *o
     run[kOrderPer - 1] = 1;
 #pragma unroll
     for (int j = kOrderPer - 2; j >= 0; j--) run[j] = cls[j] == cls[j + 1] ? run[j + 1] + 1 : 1;
+    // the call's total length (at most 2^14 rows of < 2^31: wave sums of the
+    // bits [0,16), [16,32) and [32,36) of each thread's sum fit 32 bits)
+    uint64_t ls = 0;
+#pragma unroll
+    for (int j = 0; j < kOrderPer; j++) ls += cls[j] != kNone ? (uint64_t)max(Ls[j], 0) : 0u;
+    {
+        const uint32_t lo = wave_incl_scan((uint32_t)ls & 0xFFFFu);
+        const uint32_t mid = wave_incl_scan((uint32_t)(ls >> 16) & 0xFFFFu);
+        const uint32_t hi = wave_incl_scan((uint32_t)(ls >> 32));
+        if (lane_id() == 63) lsum[w] = (int64_t)lo + ((int64_t)mid << 16) + ((int64_t)hi << 32);
+    }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kOrderPer; j++)
@@ -2356,16 +2875,71 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(const int64_t *o
 #pragma unroll
         for (int k = 0; k < 4; k++) { cnt[255 - 4 * tid - k] = acc; acc += c4[k]; }
     }
+    int64_t total = 0;
+#pragma unroll
+    for (int q = 0; q < kW; q++) total += lsum[q];
+    const uint32_t S = (uint32_t)fmax((double)kSegMin,
+                                      fmin(ceil((double)total / (double)slots), 2147483648.0));
     __syncthreads();
+    // ranks; the desired segments of the kOrderBlock longest rows
+    uint32_t rk[kOrderPer];
     uint32_t pos = 0;
 #pragma unroll
     for (int j = 0; j < kOrderPer; j++) {
+        rk[j] = 0xFFFFFFFFu;
         if (cls[j] == kNone) continue;
         if (j == 0 || cls[j] != cls[j - 1]) pos = atomicAdd(&cnt[cls[j]], run[j]);
         else pos++;
-        const uint64_t o = (uint64_t)Os[j];
-        order[pos] = make_uint4((uint32_t)(i0 + j), (uint32_t)Ls[j], (uint32_t)o, (uint32_t)(o >> 32));
+        rk[j] = pos;
+        const int32_t L = Ls[j];
+        if (pos < (uint32_t)kOrderBlock && L >= 2 * kSegMin && L <= (int32_t)TOPK_L_MAX &&
+            row_sampled(a, i0 + j, L)) {
+            const uint32_t P = min(min((uint32_t)kMaxSplit, udiv32((uint32_t)L, kSegMin)),
+                                   udiv32((uint32_t)L + S - 1u, S));
+            rinfo[pos] = P - 1u;
+        }
     }
+    __syncthreads();
+    {
+        // rank tid: extra segments E and split rows Ns up to and including it
+        // (sums of at most 63 x 1024 and 1024, packed in one word)
+        const uint32_t x = rinfo[tid];
+        const uint32_t winc = wave_incl_scan(x | (x ? 1u << 16 : 0u));
+        if (lane_id() == 63) wtot[w] = winc;
+        __syncthreads();
+        uint32_t inc = winc;
+#pragma unroll
+        for (int q = 0; q < kW; q++) inc += q < w ? wtot[q] : 0u;
+        const uint32_t E = inc & 0xFFFFu, Ns = inc >> 16;
+        const bool kept = E <= (uint32_t)extra && Ns <= max_split;
+        const uint32_t em = wave_max_to63(kept ? E : 0u);
+        if (lane_id() == 63 && em) atomicMax(&ecap_s, em);
+        __syncthreads();
+        const uint32_t ecap = ecap_s;
+        // items of the ranks before this one beyond their first, segments,
+        // slot (a kept rank's prefix never exceeds ecap)
+        const uint32_t ex = min(E - x, ecap);
+        const uint32_t xk = kept ? x : 0u;
+        rinfo[tid] = ex | (xk << 11) | ((xk ? Ns - 1u : 0u) << 17);
+    }
+    __syncthreads();
+    const uint32_t ecap = ecap_s;
+#pragma unroll
+    for (int j = 0; j < kOrderPer; j++) {
+        if (rk[j] == 0xFFFFFFFFu) continue;
+        const uint32_t k = rk[j];
+        uint32_t base = k + ecap, P = 1, slot = 0;
+        if (k < (uint32_t)kOrderBlock) {
+            const uint32_t inf = rinfo[k];
+            base = k + (inf & 0x7FFu);
+            P = ((inf >> 11) & 63u) + 1u;
+            slot = inf >> 17;
+        }
+        for (uint32_t q = 0; q < P; q++)
+            order[base + q] = order_entry((uint32_t)(i0 + j), q, P, Ls[j], (uint64_t)Os[j], slot);
+    }
+    for (uint32_t i = ecap + (uint32_t)tid; i < (uint32_t)extra; i += kOrderBlock)
+        order[n + i] = make_uint4(0x80000000u, 0u, 0u, 0u);
 }
 
 // Workspace set-up: header and zeroed per-row state (the candidate arrays
@@ -2376,6 +2950,9 @@ __global__ void ws_init_kernel(WsHeader *hdr, char *rows, uint32_t split_rows, u
         uint32_t *w = reinterpret_cast<uint32_t *>(rows + (size_t)r * kRowBlockBytes);
         for (uint32_t i = threadIdx.x; i < (kRowStateBytes + kViewHistBytes) / 4; i += blockDim.x)
             w[i] = 0;
+        uint32_t *x = reinterpret_cast<uint32_t *>(rows + (size_t)split_rows * kRowBlockBytes +
+                                                   (size_t)r * kViewHistBytes);
+        for (uint32_t i = threadIdx.x; i < kBins; i += blockDim.x) x[i] = 0;
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         hdr->split_rows = split_rows;
@@ -2403,8 +2980,8 @@ __global__ void debug_cutoff_kernel(uint32_t *out) {
 // ------------------------------------------------------------- host ----
 
 // Read-only ceiling of a call: the same work items as topk_ragged_kernel
-// (rows that the main kernel splits are cut by the same plan, every other row
-// is read by one workgroup) stream every valid score once with the same
+// (the same item table or split plan; every other row is read by one
+// workgroup) stream every valid score once with the same
 // loads (two chunks of 16-byte non-temporal loads in flight per thread) and
 // keep only the largest ascending key, which one atomic per workgroup adds
 // into out_max[r] (atomics on one address queue: one per wave made the
@@ -2415,19 +2992,26 @@ __global__ __launch_bounds__(kBlock) void read_ceiling_kernel(KArgs a, uint32_t 
     __shared__ int64_t lsum[kWaves];
     __shared__ uint32_t wmax[kWaves];
     const int tid = threadIdx.x;
-    const int p = blockIdx.x / a.n_rows;
-    const int r = blockIdx.x - p * a.n_rows;
+    const int pi = blockIdx.x / a.n_rows;
+    const bool ordered = a.order != nullptr;
+    const uint4 e = ordered ? a.order[blockIdx.x] : make_uint4(0u, 0u, 0u, 0u);
+    if (ordered && (e.x >> 31)) return;
+    const int r = ordered ? (int)(e.x & 0x3FFFu) : (int)blockIdx.x - pi * a.n_rows;
+    const int p = ordered ? (int)((e.x >> 14) & 63u) : pi;
+    const int Pe = ordered ? (int)((e.x >> 20) & 63u) + 1 : 0;
     const int32_t len_r = a.lens[r];
     const int64_t off = a.offs[r];
     const int32_t len0 = a.lens[min(tid, a.n_rows - 1)];
     const int64_t L = (int64_t)max(len_r, 0);
-    const bool sampled = L > a.K && L >= a.l_samp_min &&
-                         view_size(L, view_phase(r, a.s_log2), a.s_log2) >= a.q1;
+    const bool sampled = row_sampled(a, r, L);
     if (!sampled && p > 0) return;
     int64_t P = 1, seg = L;
     if (sampled && a.pmax > 1) {
         if ((int64_t)p * kSegMin >= L) return;
         segment_plan(a, block_total_length(a, lsum, tid < a.n_rows ? len0 : 0), L, P, seg);
+    } else if (sampled && Pe > 1) {
+        P = Pe;
+        seg = table_seg(L, Pe);
     }
     if (p >= P) return;
     const int32_t beg = (int32_t)(p * seg);
@@ -2513,8 +3097,14 @@ int32_t plan_pmax(int32_t n_rows, int cus) {
     return p;
 }
 
+// Items beyond one per row that the order pre-pass may add (segments of the
+// longest rows), and the resident workgroups whose mean work sets the
+// segment length.
+int32_t plan_extra(int cus) { return 2 * cus < kOrderExtra ? 2 * cus : kOrderExtra; }
+int32_t plan_slots(int cus) { return 2 * cus; }
+
 size_t ws_bytes(uint32_t split_rows) {
-    return kHeaderBytes + kOrderBytes + (size_t)split_rows * kRowBlockBytes;
+    return kHeaderBytes + kOrderBytes + (size_t)split_rows * (kRowBlockBytes + kViewHistBytes);
 }
 
 topk_ragged_policy default_policy() {
@@ -2677,17 +3267,24 @@ int launch_call(const float *scores, const int64_t *row_offsets, const int32_t *
     a.cap = pol.cap;
     a.spin_limit = g_spin_limit > 0 ? g_spin_limit : kSpinLimit;
     a.spin_ticks = (uint32_t)((int64_t)kSpinMicros * di.clock_khz / 1000);
+    int64_t grid = (int64_t)n_rows * pmax;
     if (pmax == 1 && n_rows <= kOrderMaxRows) {
         // more rows than resident workgroups: longest rows first, so that
-        // the last to start is short
+        // the last to start is short, the longest of them in segments
+        const int32_t extra = plan_extra(di.cus);
         uint4 *order = reinterpret_cast<uint4 *>(static_cast<char *>(workspace) + kHeaderBytes);
         hipLaunchKernelGGL(row_order_kernel, dim3(1), dim3(kOrderBlock), 0, (hipStream_t)stream,
-                           row_offsets, row_lengths, n_rows, order);
+                           a, order, extra, plan_slots(di.cus));
         if (hipGetLastError() != hipSuccess) return TOPK_ELAUNCH;
         a.order = order;
+        grid += extra;
     }
-    hipLaunchKernelGGL(topk_ragged_kernel, dim3((unsigned)(n_rows * pmax)), dim3(kBlock), 0,
-                       (hipStream_t)stream, a);
+    if (a.order)
+        hipLaunchKernelGGL(topk_ragged_kernel<true>, dim3((unsigned)grid), dim3(kBlock), 0,
+                           (hipStream_t)stream, a);
+    else
+        hipLaunchKernelGGL(topk_ragged_kernel<false>, dim3((unsigned)grid), dim3(kBlock), 0,
+                           (hipStream_t)stream, a);
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
 }
 
@@ -2720,7 +3317,7 @@ int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *
 // host it is only a stand-in for the symbol): its device address is looked up
 // once per device with hipGetSymbolAddress and kept in g_scratch_ptr.
 constexpr size_t kScratchBytes = kHeaderBytes + kOrderBytes +
-                                 (size_t)TOPK_NOALLOC_SPLIT_ROWS * kRowBlockBytes;
+                                 (size_t)TOPK_NOALLOC_SPLIT_ROWS * (kRowBlockBytes + kViewHistBytes);
 static_assert(TOPK_NOALLOC_MAX_ROWS <= kOrderMaxRows, "the order region covers every row");
 static __device__ __align__(256) char scratch[kScratchBytes];
 
@@ -2810,10 +3407,11 @@ int topk_ragged_debug_coarse(const float *x, int64_t n, uint16_t *out_c, void *s
 
 int topk_ragged_debug_read_ceiling(const float *scores, const int64_t *row_offsets,
                                    const int32_t *row_lengths, int32_t n_rows, int32_t K,
-                                   uint32_t *out_max, void *stream) {
+                                   uint32_t *out_max, void *workspace, void *stream) {
     if (n_rows < 0 || K < 1 || K > TOPK_K_MAX) return TOPK_EINVAL;
     if (n_rows == 0) return TOPK_OK;
-    if (!scores || !row_offsets || !row_lengths || !out_max) return TOPK_EINVAL;
+    if (!scores || !row_offsets || !row_lengths || !out_max || !workspace) return TOPK_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % kWorkspaceAlign) return TOPK_EINVAL;
     DeviceInfo di;
     const int st = device_info(&di);
     if (st != TOPK_OK) return st;
@@ -2835,7 +3433,20 @@ int topk_ragged_debug_read_ceiling(const float *scores, const int64_t *row_offse
     const int64_t floor_k = -(int64_t)pol.l_samp_min * K;
     a.l_samp_min = pol.l_samp_min >= 0 ? pol.l_samp_min
                                        : (int32_t)(floor_k < 0x7FFFFFFF ? floor_k : 0x7FFFFFFF);
-    hipLaunchKernelGGL(read_ceiling_kernel, dim3((unsigned)(n_rows * pmax)), dim3(kBlock), 0,
+    a.hdr = static_cast<WsHeader *>(workspace);
+    int64_t grid = (int64_t)n_rows * pmax;
+    if (pmax == 1 && n_rows <= kOrderMaxRows) {
+        // the selector's item table (its pre-pass is not part of the timing
+        // it is compared with either)
+        const int32_t extra = plan_extra(di.cus);
+        uint4 *order = reinterpret_cast<uint4 *>(static_cast<char *>(workspace) + kHeaderBytes);
+        hipLaunchKernelGGL(row_order_kernel, dim3(1), dim3(kOrderBlock), 0, (hipStream_t)stream,
+                           a, order, extra, plan_slots(di.cus));
+        if (hipGetLastError() != hipSuccess) return TOPK_ELAUNCH;
+        a.order = order;
+        grid += extra;
+    }
+    hipLaunchKernelGGL(read_ceiling_kernel, dim3((unsigned)grid), dim3(kBlock), 0,
                        (hipStream_t)stream, a, out_max);
     return hipGetLastError() == hipSuccess ? TOPK_OK : TOPK_ELAUNCH;
 }

@@ -100,7 +100,7 @@ def lib():
         L.topk_ragged_policy_for_k.restype = ctypes.c_int
         L.topk_ragged_debug_coarse.argtypes = [P, i64, P, P]
         L.topk_ragged_debug_coarse.restype = ctypes.c_int
-        L.topk_ragged_debug_read_ceiling.argtypes = [P, P, P, i32, i32, P, P]
+        L.topk_ragged_debug_read_ceiling.argtypes = [P, P, P, i32, i32, P, P, P]
         L.topk_ragged_debug_read_ceiling.restype = ctypes.c_int
         L.topk_ragged_debug_cutoffs.argtypes = [P, P]
         L.topk_ragged_debug_cutoffs.restype = ctypes.c_int
@@ -227,14 +227,17 @@ def debug_cutoffs(out_cut, stream=None) -> None:
 
 
 def debug_read_ceiling(scores, row_offsets, row_lengths, n_rows: int, K: int, out_max,
-                       stream=None) -> None:
+                       workspace, stream=None) -> None:
     """Forwards to topk_ragged_debug_read_ceiling() (read-only ceiling of a
-    call; out_max: int32 device tensor [n_rows], zeroed by the caller)."""
+    call; out_max: int32 device tensor [n_rows], zeroed by the caller;
+    workspace: an initialised workspace for at least n_rows rows)."""
     _check(lib().topk_ragged_debug_read_ceiling(_ptr(scores, torch.float32, "scores"),
                                                 _ptr(row_offsets, torch.int64, "row_offsets"),
                                                 _ptr(row_lengths, torch.int32, "row_lengths"),
                                                 n_rows, K, _ptr(out_max, torch.int32, "out_max"),
-                                                _stream(stream)), "topk_ragged_debug_read_ceiling")
+                                                _ptr(workspace, torch.uint8, "workspace"),
+                                                _stream(stream)),
+           "topk_ragged_debug_read_ceiling")
 
 
 def debug_set_spin_limit(polls: int) -> None:

@@ -506,12 +506,7 @@ def test_many_rows_halves_the_long_ones(topk):
     assert st["errors"] == 0
 
 
-@pytest.mark.parametrize("n", [1500, 16385])
-def test_many_rows_run_longest_first(topk, n):
-    """Calls whose rows each take one workgroup run them longest first
-    (1500 rows, lengths from empty to 200K in random order, stored in the
-    buffer in another order than their indices); above the order's row limit
-    (16385 short rows) they run in index order.  Same selections either way."""
+def _longest_first_workload(n):
     rng = np.random.default_rng(47 + n)
     if n <= 2000:
         lens = np.where(rng.random(n) < 0.15, rng.integers(100000, 200000, n),
@@ -524,10 +519,86 @@ def test_many_rows_run_longest_first(topk, n):
     offs = np.zeros(n, np.int64)
     offs[place] = np.concatenate([[0], np.cumsum(lens[place][:-1])])
     buf = np.concatenate([rows[r] for r in place])
-    wl = W.Workload("longest first", buf, offs, lens, 2048, "")
-    gt, st = parity(topk, wl)
+    return W.Workload("longest first", buf, offs, lens, 2048, "")
+
+
+@pytest.mark.parametrize("n", [1500, 16385])
+def test_many_rows_run_longest_first(topk, n):
+    """Calls whose rows each take one workgroup run them longest first
+    (1500 rows, lengths from empty to 200K in random order, stored in the
+    buffer in another order than their indices; the longest are cut into
+    segments); above the order's row limit (16385 short rows) they run in
+    index order.  Same selections either way."""
+    gt, st = parity(topk, _longest_first_workload(n))
     say("routes", st)
     assert st["errors"] == 0
+
+
+def _length_class(L):
+    if L < 8:
+        return max(int(L), 0)
+    e = int(L).bit_length() - 1
+    return e * 8 + ((int(L) >> (e - 3)) & 7)
+
+
+@pytest.mark.parametrize("case", ["edge mix", "1500 rows"])
+def test_item_table_cuts_the_longest_rows(topk, case):
+    """The item table of a call with more rows than resident workgroups, read
+    back from the workspace: rows longest first by length class; each row's
+    segments consecutive items with the row's length and offset; the segment
+    counts of the rule, P = min(64, L / 8192, ceil(L / S)) with S = max(8192,
+    ceil(sum L / resident workgroups)) for the 1024 longest rows, kept down the
+    order while the extra items fit the budget and the split rows the per-row
+    state; split rows in slots 0, 1, 2, ...; the rest of the table empty."""
+    import torch
+
+    wl = W.make(5) if case == "edge mix" else _longest_first_workload(1500)
+    n, K = wl.n_rows, wl.K
+    say("item table", case, "rows", n)
+    s, o, l = device_arrays(wl)
+    ws = topk.alloc_workspace(n, K)
+    run_hip(s, o, l, K, trace=False, ws=ws)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    extra, slots = min(2 * cus, 1024), 2 * cus
+    split_rows = int(ws[:1024].cpu().numpy().view(np.uint32)[1])
+    tab = ws[1024:1024 + 16 * (n + extra)].cpu().numpy().view(np.uint32).reshape(-1, 4)
+    tab = tab.astype(np.int64)
+    x, y, z, w = tab[:, 0], tab[:, 1], tab[:, 2], tab[:, 3]
+    live = (x >> 31) == 0
+    T = int(live.sum())
+    assert live[:T].all() and not live[T:].any(), "empty items must follow the last segment"
+    r, p, P = x & 0x3FFF, (x >> 14) & 63, ((x >> 20) & 63) + 1
+    off, slot = z | ((w & 0xFF) << 32), w >> 8
+    lens = wl.row_lengths.astype(np.int64)
+    S = max(8192, -(-int(np.maximum(lens, 0).sum()) // slots))
+    seen = np.zeros(n, bool)
+    i, k, E, Ns, prev_cls = 0, 0, 0, 0, 1 << 30
+    while i < T:
+        row = int(r[i])
+        assert not seen[row], f"row {row} listed twice"
+        seen[row] = True
+        Pi, Lr = int(P[i]), int(lens[row])
+        for q in range(Pi):
+            j = i + q
+            assert (r[j], p[j], P[j], y[j], off[j], slot[j]) == \
+                (row, q, Pi, Lr, wl.row_offsets[row], slot[i]), f"item {j}"
+        c = _length_class(Lr)
+        assert c <= prev_cls, f"rank {k}: class {c} after {prev_cls}"
+        prev_cls = c
+        want = 1
+        if k < 1024 and 16384 <= Lr:
+            want = min(64, Lr // 8192, -(-Lr // S))
+        E, Ns = E + want - 1, Ns + (want > 1)
+        kept = E <= extra and Ns <= split_rows
+        assert Pi == (want if kept else 1), f"rank {k} row {row} L {Lr}: P {Pi}, rule {want}"
+        if Pi > 1:
+            assert slot[i] == Ns - 1
+        i += Pi
+        k += 1
+    assert seen.all()
+    assert T - n == int((P[:T][p[:T] == 0] - 1).sum()) <= extra
+    say("split rows", int(((P[:T] > 1) & (p[:T] == 0)).sum()), "extra items", T - n, "S", S)
+    assert (P[:T] > 1).any(), "the workload should cut some rows"
 
 
 def test_segments_that_stop_waiting_build_the_view(topk):
@@ -548,6 +619,61 @@ def test_segments_that_stop_waiting_build_the_view(topk):
     assert st["wait_fallback"] > 0
 
 
+def _split_exact_workload():
+    """600 rows: 60 long ones (150K-250K, cut into segments by the item table)
+    among short ones.  Long row kinds by i % 4: 0 a decode row (primary); 1
+    the view residue N(-2, 1) (every segment overflows: the split exact
+    route); 2 a tail of ~2.5 K in the positions of one wave in one stretch
+    (a segment overflows, the row certifies: the route is abandoned); 3 low
+    values, the view residue lower still, and 10000 copies of 1.0 (overflow
+    with tau_star's bin beyond the frontier: abandoned for the re-read)."""
+    rng = np.random.default_rng(53)
+    n = 600
+    lens = rng.integers(2000, 8000, n).astype(np.int32)
+    longs = rng.choice(n, 60, replace=False)
+    lens[longs] = rng.integers(150000, 250000, 60)
+    rows = []
+    kind = {int(r): j % 4 for j, r in enumerate(longs)}
+    for i, L in enumerate(lens):
+        L = int(L)
+        x = W.decode_mixture_row(rng, L).astype(np.float32)
+        phase = int(format(i % 128, "07b")[::-1], 2)
+        k = kind.get(i, -1)
+        if k == 1:
+            x[phase::128] = rng.normal(-2.0, 1.0, x[phase::128].size).astype(np.float32)
+        elif k == 2:
+            hot = np.nonzero((np.arange(L) % 2048) < 256)[0]
+            sel = hot[(hot > L // 3) & (hot < L // 3 + 20000)]
+            x[sel] = rng.normal(4.0, 0.1, sel.size).astype(np.float32)
+        elif k == 3:
+            x = rng.normal(-3.0, 0.5, L).astype(np.float32)
+            x[rng.choice(L, 10000, replace=False)] = 1.0
+            x[phase::128] = rng.normal(-5.0, 1.0, x[phase::128].size).astype(np.float32)
+        rows.append(x)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    return W.Workload("split exact route", np.concatenate(rows), offs, lens, 2048, "")
+
+
+@pytest.mark.parametrize("spin", [0, 1], ids=["waits", "one-poll"])
+def test_split_exact_route(topk, spin):
+    """Overflowing rows cut into segments take the exact route across their
+    segments (histograms merged, tau_star published, each segment classifies
+    its own range, the last refines); rows where it does not apply abandon it
+    for the finisher.  With one poll allowed, segments stop waiting for
+    tau_star and the last arrival classifies their ranges.  Same selections
+    and traces as the oracle either way."""
+    wl = _split_exact_workload()
+    topk.debug_set_spin_limit(spin)
+    try:
+        gt, st = parity(topk, wl, where=f"split exact route, spin {spin}")
+    finally:
+        topk.debug_set_spin_limit(0)
+    say("routes", st)
+    assert st["exact_overflow"] > 0 and st["primary"] > 0 and st["reread"] > 0
+    if spin:
+        assert st["wait_fallback"] > 0
+
+
 @pytest.mark.parametrize("cfg", [2, 5])
 def test_read_ceiling_reads_every_score(topk, cfg):
     """The read-only ceiling kernel (the measurement's bound) visits every
@@ -558,7 +684,8 @@ def test_read_ceiling_reads_every_score(topk, cfg):
     say("read ceiling", wl.name)
     s, o, l = device_arrays(wl)
     out = torch.zeros(wl.n_rows, dtype=torch.int32, device="cuda")
-    topk.debug_read_ceiling(s, o, l, wl.n_rows, wl.K, out)
+    ws = topk.alloc_workspace(wl.n_rows, wl.K)
+    topk.debug_read_ceiling(s, o, l, wl.n_rows, wl.K, out, ws)
     torch.cuda.synchronize()
     got = out.cpu().numpy().view(np.uint32)
     want = np.zeros(wl.n_rows, np.uint32)
