@@ -112,13 +112,12 @@ struct RowState {
     uint32_t varrive;    // segments that have added their part of a shared view
     // The split exact route (segments that added a histogram wait for the
     // finisher's tau_star, classify their own ranges and arrive again):
-    uint32_t xtau;       // 1 << 31 | abandoned << 30 | arrivals expected << 11 | tau_star
     uint32_t ocnt;       // outputs reserved (entries with c < tau_star)
     uint32_t qcnt;       // kept entries (c == tau_star) reserved in the candidate buffer
     uint32_t arrive2;    // second arrivals
-    uint32_t xbelow;     // |E0| and |Q0| of the row, for the last arrival
-    uint32_t xeq;
-    uint64_t xmask;      // segments whose ranges the last arrival classifies
+    uint64_t xtau;       // the route word: tau_star | arrivals expected << 11 |
+                         // abandoned << 30 | 1 << 31 | |Q0| << 32 | |E0| << 48
+    uint64_t xmask;      // segments that stopped waiting
 };
 
 // Workspace header (first kHeaderBytes of the workspace).
@@ -405,7 +404,7 @@ struct alignas(16) Smem {
     uint32_t base;
     int64_t lsum[kWaves]; // per-wave partial sums of the row lengths
     uint32_t amax;        // largest ascending key among the stored entries
-    uint32_t xword;       // split exact route: the route word a waiting segment saw
+    uint64_t xword;       // split exact route: a route word
 };
 
 __device__ __forceinline__ void clear_hist(Smem &sm) {
@@ -794,15 +793,43 @@ struct Window {
     uint32_t w;
     bool fast;
     uint32_t klo, kspan, wf;
+    uint32_t imin, imax; // bounds of the live entries' indices
 };
 
-__device__ __forceinline__ Window make_window(uint64_t lo, uint64_t hi, uint32_t w) {
+// A window of keys [lo >> 32, hi >> 32] with digit shift w (the register
+// finish's single round).
+__device__ __forceinline__ Window key_window(uint64_t lo, uint64_t hi, uint32_t w) {
     Window v;
     v.lo = lo; v.hi = hi; v.w = w;
     v.fast = w >= 32 && (uint32_t)lo == 0u && (uint32_t)hi == 0xFFFFFFFFu;
     v.klo = (uint32_t)(lo >> 32);
     v.kspan = (uint32_t)(hi >> 32) - v.klo;
     v.wf = v.fast ? w - 32 : 0u;
+    v.imin = 0u; v.imax = 0xFFFFFFFFu;
+    return v;
+}
+
+// The window [lo, hi] of composite keys (kappa32 << 32 | index) with the
+// smallest shift w that fits 2048 bins.  A window inside one key is first
+// narrowed to the live indices [imin, imax], so that ties (equal keys,
+// settled by index) take as few digit rounds as the indices need.
+__device__ __forceinline__ Window make_window(uint64_t lo, uint64_t hi, uint32_t imin,
+                                              uint32_t imax) {
+    if ((lo >> 32) == (hi >> 32)) {
+        const uint64_t key = lo & 0xFFFFFFFF00000000ull;
+        lo = max(lo, key | imin);
+        hi = min(hi, key | imax);
+    }
+    const uint64_t span = hi - lo;
+    const int bits = span ? 64 - __clzll((long long)span) : 0;
+    Window v;
+    v.lo = lo; v.hi = hi;
+    v.w = bits > 11 ? (uint32_t)(bits - 11) : 0u;
+    v.fast = v.w >= 32 && (uint32_t)lo == 0u && (uint32_t)hi == 0xFFFFFFFFu;
+    v.klo = (uint32_t)(lo >> 32);
+    v.kspan = (uint32_t)(hi >> 32) - v.klo;
+    v.wf = v.fast ? v.w - 32 : 0u;
+    v.imin = imin; v.imax = imax;
     return v;
 }
 
@@ -1042,14 +1069,15 @@ __device__ __forceinline__ bool refine_round(const KArgs a, Smem &sm, uint32_t b
     // next round inside the kept bin: the 11 bits below w
     n_live = f.eq;
     const uint64_t blo = win.lo + ((uint64_t)f.bin << win.w);
-    win = make_window(blo, blo + (((uint64_t)1 << win.w) - 1), win.w > 11 ? win.w - 11 : 0u);
+    win = make_window(blo, min(blo + (((uint64_t)1 << win.w) - 1), win.hi), win.imin, win.imax);
     __syncthreads(); // sm.wc is rewritten by the next count pass
     return false;
 }
 
+// imax: the largest index an entry can have (the row length less one).
 __device__ __forceinline__ void refine(const KArgs a, Smem &sm, int r, bool segmented, uint32_t n,
                                        bool raw, uint32_t amin, uint32_t amax, uint32_t n_live,
-                                       uint32_t k) {
+                                       uint32_t k, uint32_t imax) {
     const int tid = threadIdx.x;
     const uint32_t w8 = (uint32_t)tid >> 6, lane = (uint32_t)lane_id();
     // this wave's entries: [beg, end)
@@ -1102,31 +1130,39 @@ __device__ __forceinline__ void refine(const KArgs a, Smem &sm, int r, bool segm
         return;
     }
     if (tid < 64) sm.coarse[0][tid] = 0u;
+    uint32_t imin = 0u;
     if (amax == 0u) {
-        // range pass: min/max kappa32 of the live entries
+        // range pass: min/max kappa32 and index of the live entries
         // (sm.red was reset by the caller before its barrier)
-        uint32_t kmn = ~0u, kmx = 0u;
+        uint32_t kmn = ~0u, kmx = 0u, imn = ~0u, imx = 0u;
         for (uint32_t e = beg + lane; e < end; e += 64) {
             const uint32_t kk = read_ent(sm, e, raw).kk;
-            if (kk <= khi) { kmn = min(kmn, kk); kmx = max(kmx, kk); }
+            if (kk <= khi) {
+                const uint32_t ix = sm.ci[e];
+                kmn = min(kmn, kk); kmx = max(kmx, kk);
+                imn = min(imn, ix); imx = max(imx, ix);
+            }
         }
         kmn = wave_min_to63(kmn);
         kmx = wave_max_to63(kmx);
+        imn = wave_min_to63(imn);
+        imx = wave_max_to63(imx);
         if (lane == 63) {
             atomicMin(&sm.red[0], kmn);
             atomicMax(&sm.red[1], kmx);
+            atomicMin(&sm.red[2], imn);
+            atomicMax(&sm.red[3], imx);
         }
     }
     __syncthreads();
     if (amax == 0u) {
         klo = sm.red[0];
         khi = sm.red[1];
+        imin = sm.red[2];
+        imax = sm.red[3];
     }
-    // first window: all live keys, the smallest shift that fits 2048 bins
-    const uint64_t span0 = ((uint64_t)(khi - klo) << 32) | 0xFFFFFFFFull;
-    const int bits0 = 64 - __clzll((long long)span0);
-    Window win = make_window((uint64_t)klo << 32, ((uint64_t)khi << 32) | 0xFFFFFFFFull,
-                             bits0 > 11 ? (uint32_t)(bits0 - 11) : 0u);
+    // first window: all live keys
+    Window win = make_window((uint64_t)klo << 32, ((uint64_t)khi << 32) | 0xFFFFFFFFull, imin, imax);
     int rounds_run = 0;
     for (;;) {
         const int par = rounds_run & 1;
@@ -1728,9 +1764,10 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
             f_raw = false;
             f_n = f.eq;
             // the frontier is coarse bin tau*: ascending keys from its
-            // endpoint up to below the endpoint of the bin above
+            // endpoint up; the range pass measures the keys and indices
+            // present (a bin of ties then needs only index digits)
             f_amin = bin_cutoff(f.bin);
-            f_amax = f.bin > 0 ? bin_cutoff(f.bin - 1) - 1u : 0xFFFFFFFFu;
+            f_amax = 0u;
         } else {
             route |= TOPK_ROUTE_REREAD_FLAG;
             reread_select(a, sm, r, off, L, f.bin, k_ref);
@@ -1741,7 +1778,7 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     if (n_ref) {
         reset_range(sm);
         __syncthreads();
-        refine(a, sm, r, f_seg, f_n, f_raw, f_amin, f_amax, n_ref, k_ref);
+        refine(a, sm, r, f_seg, f_n, f_raw, f_amin, f_amax, n_ref, k_ref, (uint32_t)(L - 1));
     }
     PHASE_MARK(a, 13);
     if (threadIdx.x == 0) {
@@ -1811,8 +1848,8 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
     const uint32_t klo = ~amax, khi = ~kmin;
     const uint64_t span0 = ((uint64_t)(khi - klo) << 32) | 0xFFFFFFFFull;
     const int bits0 = 64 - __clzll((long long)span0);
-    const Window win = make_window((uint64_t)klo << 32, ((uint64_t)khi << 32) | 0xFFFFFFFFull,
-                                   bits0 > 11 ? (uint32_t)(bits0 - 11) : 0u);
+    const Window win = key_window((uint64_t)klo << 32, ((uint64_t)khi << 32) | 0xFFFFFFFFull,
+                                  bits0 > 11 ? (uint32_t)(bits0 - 11) : 0u);
     if (!win.fast || win.kspan == 0xFFFFFFFFu) return false;
     PHASE_MARK(a, 8);
     // histogram of the live keys (sm.hist and its group sums are clear);
@@ -1935,12 +1972,10 @@ __device__ __forceinline__ void reset_row_state(RowState *rs, bool x = true) {
     __hip_atomic_store(&rs->taus, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->varrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (!x) return;
-    __hip_atomic_store(&rs->xtau, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&rs->xtau, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->ocnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->qcnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->arrive2, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&rs->xbelow, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&rs->xeq, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&rs->xmask, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -1957,7 +1992,7 @@ __device__ __forceinline__ void reset_row_state(RowState *rs, bool x = true) {
 // into the candidate buffer (Q0), at slots reserved with one atomic per
 // segment from its own histogram's counts.  The last to finish refines Q0.
 
-constexpr uint32_t kXGo = 0x80000000u, kXAbandon = 0x40000000u;
+constexpr uint64_t kXGo = 0x80000000u, kXAbandon = 0x40000000u;
 
 // Entries of h in bins < t and in bin t, into sm.cnt0 and sm.cnt (zero
 // before a preceding barrier).  Ends with a barrier.
@@ -1996,8 +2031,9 @@ __device__ __forceinline__ void classify_range(const KArgs a, Smem &sm, int r, i
     int32_t *oi = a.out_idx + (int64_t)r * a.K;
     float *ov = a.out_val + (int64_t)r * a.K;
     static_assert(kVec * 4 <= 16 && kWaves * 64 * 16 < 65536, "packed counts");
-    stream_row<false>(a.scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                   int32_t hi, bool edge, int32_t mv) {
+    stream_row<false>(a.scores, off, beg, end, [&](const f4 *x, const int32_t *i0,
+                                                            int32_t lo, int32_t hi, bool edge,
+                                                            int32_t mv) {
         uint32_t mlt = 0, meq = 0;
 #pragma unroll
         for (int m = 0; m < kVec; m++) if (m < mv) {
@@ -2087,6 +2123,7 @@ __device__ __forceinline__ void classify_own_range(const KArgs a, Smem &sm, int 
                                                 __HIP_MEMORY_SCOPE_AGENT) : 0u;
     }
     __syncthreads();
+    PHASE_MARK(a, 31);
     const uint32_t glt = sm.flag, geq = sm.base;
     const uint32_t key_hi = ts > 0 ? bin_cutoff(ts - 1u) : 0xFFFFFFFFu, key_lo = bin_cutoff(ts);
     classify_range(a, sm, r, off, beg, end, key_lo, key_hi, n_lt, n_eq, glt, geq, gc);
@@ -2157,7 +2194,7 @@ __device__ __forceinline__ void classify_stored(const KArgs a, Smem &sm, int r, 
 // bit in xmask is set first).  Returns the route word for the last arrival,
 // 0 for the others.  Each wave's stores complete before the barrier that
 // precedes the arrival (as for the first arrival).
-__device__ __forceinline__ uint32_t arrive_again(Smem &sm, RowState *rs, int p, uint32_t xt0) {
+__device__ __forceinline__ uint64_t arrive_again(Smem &sm, RowState *rs, int p, uint64_t xt0) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -2169,11 +2206,11 @@ __device__ __forceinline__ uint32_t arrive_again(Smem &sm, RowState *rs, int p, 
                                                     __HIP_MEMORY_SCOPE_AGENT);
         // the finisher publishes the route word before its own arrival, so a
         // last arrival always sees it
-        const uint32_t xt = __hip_atomic_load(&rs->xtau, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        sm.flag = ((xt & kXGo) && old + 1u == ((xt >> 11) & 0xFFu)) ? xt : 0u;
+        const uint64_t xt = __hip_atomic_load(&rs->xtau, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.xword = ((xt & kXGo) && old + 1u == ((uint32_t)(xt >> 11) & 0xFFu)) ? xt : 0ull;
     }
     __syncthreads();
-    return sm.flag;
+    return sm.xword;
 }
 
 // The last arrival of the split exact route: loads Q0 and refines it for the
@@ -2181,37 +2218,49 @@ __device__ __forceinline__ uint32_t arrive_again(Smem &sm, RowState *rs, int p, 
 // false, with nothing done, when a segment stopped waiting (its range is not
 // classified): the caller then runs the whole row's exact route, which
 // rewrites every output; sm.wk[2] and sm.wk[3] hold C(tau1) and C(tau0).
-__device__ __forceinline__ bool split_exact_final(const KArgs a, Smem &sm, int r, int64_t nv,
-                                                  RowState *rs, uint64_t *gc, uint32_t xt) {
+__device__ __forceinline__ bool split_exact_final(const KArgs a, Smem &sm, int r, int64_t L,
+                                                  int64_t nv, RowState *rs, uint64_t *gc,
+                                                  uint64_t xt) {
     const int tid = threadIdx.x;
-    const uint32_t ts = xt & 0x7FFu;
+    const uint32_t ts = (uint32_t)xt & 0x7FFu;
+    const uint32_t eq = min((uint32_t)(xt >> 32) & 0x3FFFu, (uint32_t)kFront);
+    const uint32_t below = (uint32_t)(xt >> 48) & 0x3FFFu;
+    // the segment mask and the counts (|E0|, |Q0| and tau_star came with the
+    // route word)
     if (tid == 0) {
-        sm.wc[0] = __hip_atomic_load(&rs->xbelow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        sm.wc[1] = __hip_atomic_load(&rs->xeq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t m = __hip_atomic_load(&rs->xmask, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        sm.wk[0] = (uint32_t)m;
-        sm.wk[1] = (uint32_t)(m >> 32);
         const uint64_t cc = __hip_atomic_load(&rs->counts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.wk[0] = m != 0ull;
         sm.wk[2] = (uint32_t)cc;
         sm.wk[3] = (uint32_t)(cc >> 32);
     }
     __syncthreads();
-    const uint32_t below = sm.wc[0], eq = sm.wc[1];
-    if (sm.wk[0] | sm.wk[1]) return false;
+    if (sm.wk[0]) return false;
     const uint32_t C1 = sm.wk[2], C0 = sm.wk[3];
-    // Q0: the kept entries, as kappa32 keys
-    for (uint32_t e = (uint32_t)tid; e < min(eq, (uint32_t)kFront); e += kBlock) {
-        const uint64_t v = __hip_atomic_load(&gc[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        sm.ci[e] = (uint32_t)v;
-        sm.ck[e] = ~asc_key((uint32_t)(v >> 32));
+    // Q0 as kappa32 keys, four loads in flight per thread
+    for (uint32_t e0 = 0; e0 < eq; e0 += 4 * kBlock) {
+        uint64_t q[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const uint32_t e = e0 + (uint32_t)(j * kBlock + tid);
+            q[j] = e < eq ? __hip_atomic_load(&gc[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                          : 0ull;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const uint32_t e = e0 + (uint32_t)(j * kBlock + tid);
+            if (e < eq) {
+                sm.ci[e] = (uint32_t)q[j];
+                sm.ck[e] = ~asc_key((uint32_t)(q[j] >> 32));
+            }
+        }
     }
     clear_hist(sm);
     reset_range(sm);
     if (tid == 0) sm.opos = 0;
     __syncthreads();
     const uint32_t amin = bin_cutoff(ts);
-    const uint32_t amax = ts > 0 ? bin_cutoff(ts - 1u) - 1u : 0xFFFFFFFFu;
-    refine(a, sm, r, false, eq, false, amin, amax >= amin ? amax : 0u, eq, (uint32_t)a.K - below);
+    refine(a, sm, r, false, eq, false, amin, 0u, eq, (uint32_t)a.K - below, (uint32_t)(L - 1));
     PHASE_MARK(a, 13);
     if (tid == 0) {
         atomicAdd(&a.hdr->stats[TOPK_ROUTE_EXACT_OVERFLOW], 1u);
@@ -2271,6 +2320,7 @@ topk_ragged_kernel(KArgs a) {
     const float *row = a.scores + off;
     PHASE_MARK(a, 0);
     PHASE_WORD(a, 6, (uint64_t)__smid());
+    PHASE_WORD(a, 7, (uint64_t)p | ((uint64_t)r << 32)); // (segments filled in later)
 
     // Workspace check: a split plan needs per-row state for every row.
     const bool ws_bad = (hw.x != kMagic) | ((uint32_t)a.n_rows > hw.z) |
@@ -2573,7 +2623,7 @@ topk_ragged_kernel(KArgs a) {
                 // (bounded as the boundary wait; after it the last arrival
                 // classifies this range), classify this range, arrive again.
                 if (tid == 0) {
-                    uint32_t v = 0;
+                    uint64_t v = 0;
                     const uint64_t t_wait = wall_clock64();
                     for (int spin = 0; spin < a.spin_limit; spin++) {
                         v = __hip_atomic_load(&rs->xtau, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2584,16 +2634,20 @@ topk_ragged_kernel(KArgs a) {
                     if (!(v & kXGo)) atomicAdd(&a.hdr->stats[kStatWaitFallback], 1u);
                 }
                 __syncthreads();
-                const uint32_t xv = sm.xword;
+                PHASE_MARK(a, 29);
+                const uint64_t xv = sm.xword;
                 if ((xv & (kXGo | kXAbandon)) == kXGo)
-                    classify_own_range(a, sm, r, off, beg, end, sm.hist, xv & 0x7FFu, rs, gc);
-                const uint32_t xt = arrive_again(sm, rs, p, xv);
+                    classify_own_range(a, sm, r, off, beg, end, sm.hist,
+                                              (uint32_t)xv & 0x7FFu, rs, gc);
+                PHASE_MARK(a, 27);
+                const uint64_t xt = arrive_again(sm, rs, p, xv);
+                PHASE_MARK(a, 28);
                 if (!xt) return;
                 if (xt & kXAbandon) {
                     if (tid == 0) reset_row_state(rs);
                     return;
                 }
-                if (split_exact_final(a, sm, r, nv, rs, gc, xt)) {
+                if (split_exact_final(a, sm, r, L, nv, rs, gc, xt)) {
                     PHASE_MARK(a, 5);
                     return;
                 }
@@ -2693,26 +2747,28 @@ topk_ragged_kernel(KArgs a) {
                 xexpect = nx + (pushed ? 0u : 1u);
                 if (dist) {
                     const Find f = sm.find[0];
-                    if (tid == 0) {
-                        __hip_atomic_store(&rs->xbelow, f.below, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(&rs->xeq, f.eq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(&rs->xtau, kXGo | (xexpect << 11) | f.bin, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                    }
+                    if (tid == 0)
+                        __hip_atomic_store(&rs->xtau,
+                                           kXGo | ((uint64_t)xexpect << 11) | f.bin |
+                                               ((uint64_t)f.eq << 32) | ((uint64_t)f.below << 48),
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     PHASE_MARK(a, 4);
                     classify_stored(a, sm, r, rs, gc, vi, vk, stored, f.bin);
+                    PHASE_MARK(a, 26);
                     if (pushed) classify_own_range(a, sm, r, off, beg, end, sm.ck, f.bin, rs, gc);
-                    const uint32_t xt = arrive_again(sm, rs, p, kXGo);
+                    PHASE_MARK(a, 27);
+                    const uint64_t xt = arrive_again(sm, rs, p, kXGo);
+                    PHASE_MARK(a, 28);
                     if (!xt) return;
-                    if (split_exact_final(a, sm, r, nv, rs, gc, xt)) {
+                    if (split_exact_final(a, sm, r, L, nv, rs, gc, xt)) {
                         PHASE_MARK(a, 5);
                         return;
                     }
                     redo = true;
                 } else if (tid == 0) {
                     // any other route runs here, on this workgroup
-                    __hip_atomic_store(&rs->xtau, kXGo | kXAbandon | (xexpect << 11), __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(&rs->xtau, kXGo | kXAbandon | ((uint64_t)xexpect << 11),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
             __syncthreads();
@@ -2761,7 +2817,8 @@ topk_ragged_kernel(KArgs a) {
         }
         __syncthreads();
     }
-    finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored, have_hist);
+    finish_row(a, sm, r, off, L, nv, sampled, C0, C1, incomplete, segmented, nstored,
+                      have_hist);
     PHASE_MARK(a, 5);
 
     // the row state is reset once every segment is done with it
