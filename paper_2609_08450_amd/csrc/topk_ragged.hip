@@ -592,8 +592,13 @@ __device__ __forceinline__ void collect_range(Smem &sm, const float *scores, int
 // Each element costs one compare; a wave-wide ballot places the hits with no
 // atomics, and sm.cnt gets C(tau1).  A wave whose region overflows sets
 // sm.incomplete and stops (sm.cnt is then partial; the caller re-counts by
-// re-reading).  The endpoints are read from sm after prologue() has run.
-template <class Pro>
+// re-reading) -- or, with kHistOver, goes on to the end of the range adding
+// each hit its region cannot keep into the coarse histogram sm.hist2 (clear
+// before a barrier that precedes the first chunk's consumption): the stored
+// entries and sm.hist2 then count every hit, so sm.cnt is exact and the
+// coarse histogram of the range is exact in bins 0..tau1 without a re-read.
+// The endpoints are read from sm after prologue() has run.
+template <bool kHistOver, class Pro>
 __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, int64_t off,
                                                int32_t beg, int32_t end, Pro &&prologue) {
     const int w = threadIdx.x >> 6;
@@ -626,6 +631,18 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
                         if constexpr (kEdge) hit[c] = h1 && in_window(i0[m] + c, lo, hi);
                         mk[c] = __ballot(hit[c]);
                     }
+                    if constexpr (kHistOver) {
+                        if (cur >= (uint32_t)kWaveCap) { // (wave-uniform)
+                            // region full: the hits are only counted
+#pragma unroll
+                            for (int c = 0; c < 4; c++) {
+                                if (hit[c]) atomicAdd(&sm.hist2[coarse_bin(x[m][c])], 1u);
+                                cur += (uint32_t)__popcll(mk[c]);
+                            }
+                            continue;
+                        }
+                    }
+                    const uint32_t cur0 = cur;
 #pragma unroll
                     for (int c = 0; c < 4; c++) {
                         // slot kWaveCap of the region absorbs hits past its
@@ -637,6 +654,21 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
                         wi[d] = (uint32_t)(i0[m] + c);
                         wk[d] = fbits(x[m][c]);
                         cur += (uint32_t)__popcll(mk[c]);
+                    }
+                    if constexpr (kHistOver) {
+                        if (cur > (uint32_t)kWaveCap) { // (wave-uniform, once per wave)
+                            // the hits of this vector past the capacity
+                            uint32_t run_c = cur0;
+#pragma unroll
+                            for (int c = 0; c < 4; c++) {
+                                const uint32_t rk = __builtin_amdgcn_mbcnt_hi(
+                                    (uint32_t)(mk[c] >> 32),
+                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mk[c], run_c));
+                                if (hit[c] && rk >= (uint32_t)kWaveCap)
+                                    atomicAdd(&sm.hist2[coarse_bin(x[m][c])], 1u);
+                                run_c += (uint32_t)__popcll(mk[c]);
+                            }
+                        }
                     }
                 }
             };
@@ -652,7 +684,8 @@ __device__ __forceinline__ void phase2_collect(Smem &sm, const float *scores, in
         prologue,
         // a wave whose region has overflowed stops: the segment's entries
         // will not be used, and both counts are then taken by a re-read
-        [&]() { return cur > (uint32_t)kWaveCap; });
+        // (with kHistOver no wave stops)
+        [&]() { return !kHistOver && cur > (uint32_t)kWaveCap; });
     if ((threadIdx.x & 63) == 0) {
         sm.wcnt[w] = cur;
         atomicAdd(&sm.cnt, cur);
@@ -2380,6 +2413,11 @@ topk_ragged_kernel(KArgs a) {
         // A row has at most ceil(L / kSegMin) segments (see below).
         if ((int64_t)p * kSegMin >= L) return;
         clear_hist(sm);
+        if constexpr (kOrdered) {
+            // the hits Phase 2's regions cannot keep
+            uint4 *h2 = reinterpret_cast<uint4 *>(sm.hist2);
+            for (int i = tid; i < kBins / 4; i += kBlock) h2[i] = make_uint4(0, 0, 0, 0);
+        }
         if (tid == 0) { sm.cnt = 0; sm.cnt0 = 0; sm.incomplete = 0; sm.amax = 0; }
         // Segment 0 reads the view; its loads go out first, the segment plan
         // and the first chunk follow, and the view is histogrammed with that
@@ -2422,7 +2460,7 @@ topk_ragged_kernel(KArgs a) {
         // sharing the GPU can keep the publishing segment from running, and
         // with a shared view any segment may wait for one dispatched after it.
         PHASE_MARK(a, 16);
-        phase2_collect(sm, a.scores, off, beg, end, [&]() {
+        phase2_collect<kOrdered>(sm, a.scores, off, beg, end, [&]() {
             bool have = false; // endpoints in sm
             if (coop) {
                 have = coop_view_finish(a, sm, r, row, k0, k1, xs, rs, vh, P);
@@ -2545,16 +2583,34 @@ topk_ragged_kernel(KArgs a) {
             if (__builtin_expect(incomplete, 0)) {
                 __syncthreads(); // every thread has read sm.cnt
                 if (tid == 0) sm.cnt = 0; // (sm.cnt0 is still zero)
-                if (!split || kOrdered) clear_hist(sm);
-                __syncthreads();
-                if (split && !kOrdered) {
-                    count_range(sm, a.scores, off, beg, end, sm.cut0, sm.cut1);
-                } else {
-                    exact_hist(a, sm, off, beg, end);
+                if constexpr (kOrdered) {
+                    // Phase 2 went on past the overflow: its stored entries
+                    // plus the hits in sm.hist2 make the coarse histogram,
+                    // exact in bins 0..tau1 (enough for C(tau0), C(tau1), and
+                    // for tau_star when C(tau1) >= K)
+                    reinterpret_cast<uint4 *>(sm.hist)[tid] =
+                        reinterpret_cast<const uint4 *>(sm.hist2)[tid];
+                    __syncthreads();
+                    const uint32_t w8 = (uint32_t)tid >> 6;
+                    const uint32_t nw = min(sm.wcnt[w8], (uint32_t)kWaveCap);
+                    for (uint32_t e = (uint32_t)lane_id(); e < nw; e += 64)
+                        atomicAdd(&sm.hist[coarse_bin(__builtin_bit_cast(
+                                      float, sm.ck[w8 * kWaveStride + e]))], 1u);
+                    __syncthreads();
                     hist_counts(sm, sm.tau0, sm.tau1);
+                } else {
+                    if (!split) clear_hist(sm);
+                    __syncthreads();
+                    if (split) {
+                        count_range(sm, a.scores, off, beg, end, sm.cut0, sm.cut1);
+                    } else {
+                        exact_hist(a, sm, off, beg, end);
+                        hist_counts(sm, sm.tau0, sm.tau1);
+                    }
                 }
                 if (!split) {
-                    have_hist = true;
+                    // (a histogram exact only up to tau1 serves when C(tau1) >= K)
+                    have_hist = !kOrdered || sm.cnt >= (uint32_t)a.K;
                 } else if (kOrdered) {
                     const uint4 h = reinterpret_cast<const uint4 *>(sm.hist)[tid];
                     uint32_t *d = xh + 4 * tid;

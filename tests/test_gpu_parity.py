@@ -437,14 +437,16 @@ def test_parity_per_k_policy(topk, K):
         assert st["reread"] >= 1
 
 
-def test_single_workgroup_rows_with_an_overflowed_region(topk):
-    """Rows on one workgroup each (the call has too many rows to split) whose
-    admitted tail lies in positions one wave streams: that wave's region
-    overflows, so C(tau0) comes from the coarse-histogram pass; rows whose
-    proposal certifies re-collect their frontier, overflowing ones reuse the
-    histogram for the exact route."""
+@pytest.mark.parametrize("n", [400, 600])
+def test_single_workgroup_rows_with_an_overflowed_region(topk, n):
+    """Rows whose admitted tail lies in positions one wave streams: that
+    wave's region overflows, so C(tau0) comes from a coarse histogram (a
+    re-read of the row; in a call run from the item table, 600 rows of one
+    workgroup each, Phase 2 goes on and counts the hits its region cannot
+    keep); rows whose proposal certifies re-collect their frontier,
+    overflowing ones reuse the histogram for the exact route."""
     rng = np.random.default_rng(31)
-    L, n = 24576, 400
+    L = 24576
     hot = (np.arange(L) % 2048) < 256   # the positions of wave 0 in every chunk
     rows = []
     for i in range(n):
