@@ -15,7 +15,10 @@
  * behind a ragged-row dispatcher: rows with L <= K are written directly,
  * short rows run on one workgroup, long rows are split across several
  * workgroups whose admitted candidates are merged by the last one to finish
- * (Section 4.5, eq:method:split-local, eq:method:split-reduce).
+ * (Section 4.5, eq:method:split-local, eq:method:split-reduce); a call with
+ * more rows than resident workgroups runs its rows longest first and splits
+ * only the longest, and a split row whose candidates overflow takes the exact
+ * coarse recovery across its segments.
  *
  * Semantics (Section 2.1 operator contract, with the choices the paper leaves
  * open fixed as follows):
@@ -98,7 +101,10 @@ typedef struct topk_ragged_policy {
 typedef struct topk_ragged_stats {
     uint64_t route[6];     /* indexed by TOPK_ROUTE_* (flag stripped) */
     uint64_t reread;       /* rows that took the re-read fallback */
-    uint64_t wait_fallback;/* split segments that recomputed the view locally */
+    uint64_t wait_fallback;/* split segments that stopped waiting: for the
+                              boundaries (they recompute the view locally),
+                              or for tau_star of the split exact route (the
+                              last segment then runs the row's exact route) */
     uint64_t errors;       /* rejected on the device: one per call with a bad
                               workspace, one per row longer than TOPK_L_MAX */
 } topk_ragged_stats;
@@ -127,9 +133,10 @@ int topk_ragged_policy_for_k(int32_t K, topk_ragged_policy *out);
  * requirements"), and the plan that sizes it is fixed before capture from the
  * row capacity and the device (Section 5.5, "Shape-stable dispatch"): the
  * size depends only on (max_rows, K, device), never on row lengths.  Per-row
- * state is kept only for rows split across workgroups, and at most
- * 4 x (compute units) rows are ever split.  Pure host computation; returns 0
- * for invalid arguments (max_rows < 0, K outside [1, TOPK_K_MAX]). */
+ * state (about 72 KB) is kept only for rows split across workgroups, and at
+ * most min(max_rows, 4 x (compute units)) rows of a call are split.  Pure host
+ * computation; returns 0 for invalid arguments (max_rows < 0, K outside
+ * [1, TOPK_K_MAX]). */
 size_t topk_ragged_workspace_size(int32_t max_rows, int32_t K);
 
 /* One-time initialisation of a workspace of `bytes` bytes (enqueued on
@@ -166,8 +173,10 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
  * Row lengths and offsets stay on the device; the launch geometry depends
  * only on (n_rows, K, device).  A call of more than 2 x CUs and at most
  * 16384 rows enqueues a one-workgroup pre-pass before the main kernel: it
- * writes the order of the rows, longest first, into the workspace.  If the workspace is invalid for n_rows the
- * kernel writes -1 / -inf to every output and counts an error in the stats.
+ * writes the work items into the workspace, rows longest first, the longest
+ * of them cut into segments (at most 2 x CUs more items; row offsets below
+ * 2^40 elements).  If the workspace is invalid for n_rows the kernel writes
+ * -1 / -inf to every output and counts an error in the stats.
  * Returns TOPK_OK or an error code; nothing is enqueued on an argument
  * error. */
 int topk_ragged(const float *scores, const int64_t *row_offsets, const int32_t *row_lengths,
@@ -193,23 +202,23 @@ int topk_ragged_ex(const float *scores, const int64_t *row_offsets, const int32_
                    int32_t n_rows, int32_t K, int32_t *out_idx, float *out_val, void *workspace,
                    const topk_ragged_policy *policy, int32_t *row_trace, void *stream);
 
-/* Limits of topk_ragged_noalloc: most rows per call, and most rows a call may
- * have for its long rows to be split across workgroups (a call of more rows
- * runs each row on one workgroup, as topk_ragged does above 2 x CUs rows). */
+/* Limits of topk_ragged_noalloc: most rows per call, and most rows with
+ * per-row state: a call of at most that many rows may split any row, a larger
+ * one splits at most that many of its longest rows. */
 #define TOPK_NOALLOC_MAX_ROWS 16384
 #define TOPK_NOALLOC_SPLIT_ROWS 64
 
 /* topk_ragged without a workspace argument, for callers that cannot allocate
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc).  The library keeps the workspace in a device array of about
- * 4.5 MB per GPU (header, row-order region, per-row state for
+ * 5.0 MB per GPU (header, work-item region, per-row state for
  * TOPK_NOALLOC_SPLIT_ROWS split rows), held until the process ends; this call
  * allocates nothing and calls no allocating routine.  The first call on a
  * device looks up the array's address and enqueues its one-time
  * initialisation on `stream` ahead of the call.  Arguments, outputs and
  * results are those of topk_ragged with the per-K policy: the same (index,
- * value) sets; calls of more than TOPK_NOALLOC_SPLIT_ROWS rows do not split
- * rows.  Every call on one GPU uses that GPU's array: calls that overlap on
+ * value) sets; a call of more than TOPK_NOALLOC_SPLIT_ROWS rows splits at most
+ * that many rows.  Every call on one GPU uses that GPU's array: calls that overlap on
  * one GPU (concurrent streams or threads) race and must not be made; the
  * kernels leave the array's state zeroed for the next call.  Returns
  * TOPK_EWORKSPACE for n_rows > TOPK_NOALLOC_MAX_ROWS, otherwise as

@@ -2268,6 +2268,7 @@ __device__ __forceinline__ bool split_exact_final(const KArgs a, Smem &sm, int r
         sm.wk[3] = (uint32_t)(cc >> 32);
     }
     __syncthreads();
+    PHASE_MARK(a, 8);
     if (sm.wk[0]) return false;
     const uint32_t C1 = sm.wk[2], C0 = sm.wk[3];
     // Q0 as kappa32 keys, four loads in flight per thread
@@ -2292,6 +2293,7 @@ __device__ __forceinline__ bool split_exact_final(const KArgs a, Smem &sm, int r
     reset_range(sm);
     if (tid == 0) sm.opos = 0;
     __syncthreads();
+    PHASE_MARK(a, 9);
     const uint32_t amin = bin_cutoff(ts);
     refine(a, sm, r, false, eq, false, amin, 0u, eq, (uint32_t)a.K - below, (uint32_t)(L - 1));
     PHASE_MARK(a, 13);
