@@ -2902,9 +2902,13 @@ __device__ __forceinline__ uint32_t length_class(int32_t L) {
 // sort of the rows by length class, longest first (any order within a
 // class), then the work items in that order into order[0, n + extra).
 // One workgroup; n <= kOrderMaxRows, extra <= kOrderExtra.  Thread t takes
-// rows [kOrderPer t, kOrderPer (t + 1)), and a run of equal classes among
-// them takes one LDS atomic: rows of similar length would otherwise all add
-// into one counter at once.
+// rows [R t, R (t + 1)), and a run of equal classes among them takes one LDS
+// atomic: rows of similar length would otherwise all add into one counter at
+// once.  R = 1 when the rows fit the workgroup (each row's rank costs its
+// thread a dependent LDS atomic: a call of 1024 rows of random lengths spent
+// 3.5 us ranking on one wave), else kOrderPer, which places each wave's 1024
+// rows of a class as one block (smaller blocks made the chunked-prefill block
+// 2 % slower: see the order's measurements).
 //
 // Splitting (KV-split mapping, Section 4.5, for calls too large to split
 // every row): a sampled row among the kOrderBlock longest gets
@@ -2915,8 +2919,10 @@ __device__ __forceinline__ uint32_t length_class(int32_t L) {
 // within the workspace's per-row state (slot k for the k-th split row);
 // every later row runs whole.  A row's segments are consecutive items, and
 // items past the last are marked empty.
+template <int R>
 __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *order,
                                                                 int32_t extra, int32_t slots) {
+    static_assert(R == 1 || R == kOrderPer, "rows per thread");
     constexpr uint32_t kNone = 256; // class of a position past the last row
     constexpr int kW = kOrderBlock / 64;
     __shared__ uint32_t cnt[256];
@@ -2927,16 +2933,17 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
     const int n = a.n_rows;
     const int tid = threadIdx.x;
     const int w = tid >> 6;
-    const int i0 = tid * kOrderPer;
+    const int i0 = tid * R;
     if (tid < 256) cnt[tid] = 0;
     if (tid == 0) ecap_s = 0;
     rinfo[tid] = 0;
     const uint32_t max_split = a.hdr->split_rows;
     int32_t Ls[kOrderPer];
     int64_t Os[kOrderPer]; // loaded with the lengths: one round trip to memory
-    // (16-byte loads where the arrays allow: each thread's rows are
-    // contiguous, so the lanes of one load are 64 bytes apart)
-    const bool vec = ((reinterpret_cast<uintptr_t>(a.lens) |
+    // (16-byte loads where the arrays allow and a thread takes kOrderPer
+    // rows: its rows are contiguous, so the lanes of one load are 64 bytes
+    // apart)
+    const bool vec = R == kOrderPer && ((reinterpret_cast<uintptr_t>(a.lens) |
                        reinterpret_cast<uintptr_t>(a.offs)) & 15u) == 0 && i0 + kOrderPer <= n;
     if (vec) {
         const int4 *l4 = reinterpret_cast<const int4 *>(a.lens + i0);
@@ -2954,13 +2961,14 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
     } else {
 #pragma unroll
         for (int j = 0; j < kOrderPer; j++) {
-            Ls[j] = i0 + j < n ? a.lens[i0 + j] : 0;
-            Os[j] = i0 + j < n ? a.offs[i0 + j] : 0;
+            Ls[j] = j < R && i0 + j < n ? a.lens[i0 + j] : 0;
+            Os[j] = j < R && i0 + j < n ? a.offs[i0 + j] : 0;
         }
     }
     uint32_t cls[kOrderPer], run[kOrderPer]; // run[j]: rows of j's run from j on
 #pragma unroll
-    for (int j = 0; j < kOrderPer; j++) cls[j] = i0 + j < n ? length_class(Ls[j]) : kNone;
+    for (int j = 0; j < kOrderPer; j++)
+        cls[j] = j < R && i0 + j < n ? length_class(Ls[j]) : kNone;
     run[kOrderPer - 1] = 1;
 #pragma unroll
     for (int j = kOrderPer - 2; j >= 0; j--) run[j] = cls[j] == cls[j + 1] ? run[j + 1] + 1 : 1;
@@ -2995,6 +3003,7 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
     for (int q = 0; q < kW; q++) total += lsum[q];
     const uint32_t S = (uint32_t)fmax((double)kSegMin,
                                       fmin(ceil((double)total / (double)slots), 2147483648.0));
+    const float rS = __builtin_amdgcn_rcpf((float)S);
     __syncthreads();
     // ranks; the desired segments of the kOrderBlock longest rows
     uint32_t rk[kOrderPer];
@@ -3009,8 +3018,12 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
         const int32_t L = Ls[j];
         if (pos < (uint32_t)kOrderBlock && L >= 2 * kSegMin && L <= (int32_t)TOPK_L_MAX &&
             row_sampled(a, i0 + j, L)) {
-            const uint32_t P = min(min((uint32_t)kMaxSplit, udiv32((uint32_t)L, kSegMin)),
-                                   udiv32((uint32_t)L + S - 1u, S));
+            // ceil(L / S) from a single-precision quotient (off by at most
+            // one: L / S < 2^18) and one exact integer correction
+            uint32_t q = (uint32_t)ceilf((float)L * rS);
+            if ((uint64_t)q * S < (uint64_t)L) q++;
+            else if (q > 1u && (uint64_t)(q - 1u) * S >= (uint64_t)L) q--;
+            const uint32_t P = min(min((uint32_t)kMaxSplit, (uint32_t)L / (uint32_t)kSegMin), q);
             rinfo[pos] = P - 1u;
         }
     }
@@ -3388,8 +3401,12 @@ int launch_call(const float *scores, const int64_t *row_offsets, const int32_t *
         // the last to start is short, the longest of them in segments
         const int32_t extra = plan_extra(di.cus);
         uint4 *order = reinterpret_cast<uint4 *>(static_cast<char *>(workspace) + kHeaderBytes);
-        hipLaunchKernelGGL(row_order_kernel, dim3(1), dim3(kOrderBlock), 0, (hipStream_t)stream,
-                           a, order, extra, plan_slots(di.cus));
+        if (n_rows <= kOrderBlock)
+            hipLaunchKernelGGL(row_order_kernel<1>, dim3(1), dim3(kOrderBlock), 0,
+                               (hipStream_t)stream, a, order, extra, plan_slots(di.cus));
+        else
+            hipLaunchKernelGGL(row_order_kernel<kOrderPer>, dim3(1), dim3(kOrderBlock), 0,
+                               (hipStream_t)stream, a, order, extra, plan_slots(di.cus));
         if (hipGetLastError() != hipSuccess) return TOPK_ELAUNCH;
         a.order = order;
         grid += extra;
@@ -3555,8 +3572,12 @@ int topk_ragged_debug_read_ceiling(const float *scores, const int64_t *row_offse
         // it is compared with either)
         const int32_t extra = plan_extra(di.cus);
         uint4 *order = reinterpret_cast<uint4 *>(static_cast<char *>(workspace) + kHeaderBytes);
-        hipLaunchKernelGGL(row_order_kernel, dim3(1), dim3(kOrderBlock), 0, (hipStream_t)stream,
-                           a, order, extra, plan_slots(di.cus));
+        if (n_rows <= kOrderBlock)
+            hipLaunchKernelGGL(row_order_kernel<1>, dim3(1), dim3(kOrderBlock), 0,
+                               (hipStream_t)stream, a, order, extra, plan_slots(di.cus));
+        else
+            hipLaunchKernelGGL(row_order_kernel<kOrderPer>, dim3(1), dim3(kOrderBlock), 0,
+                               (hipStream_t)stream, a, order, extra, plan_slots(di.cus));
         if (hipGetLastError() != hipSuccess) return TOPK_ELAUNCH;
         a.order = order;
         grid += extra;
