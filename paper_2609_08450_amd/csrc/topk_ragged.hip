@@ -2927,6 +2927,8 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
     constexpr int kW = kOrderBlock / 64;
     __shared__ uint32_t cnt[256];
     __shared__ uint32_t rinfo[kOrderBlock]; // by rank: extra segments, then the plan
+    __shared__ uint32_t rrow[kOrderBlock];  // by rank: the row and its length
+    __shared__ int32_t rlen[kOrderBlock];
     __shared__ uint32_t wtot[kW];
     __shared__ int64_t lsum[kW];
     __shared__ uint32_t ecap_s;
@@ -2936,7 +2938,7 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
     const int i0 = tid * R;
     if (tid < 256) cnt[tid] = 0;
     if (tid == 0) ecap_s = 0;
-    rinfo[tid] = 0;
+    rlen[tid] = 0;
     const uint32_t max_split = a.hdr->split_rows;
     int32_t Ls[kOrderPer];
     int64_t Os[kOrderPer]; // loaded with the lengths: one round trip to memory
@@ -3015,19 +3017,26 @@ __global__ __launch_bounds__(kOrderBlock) void row_order_kernel(KArgs a, uint4 *
         if (j == 0 || cls[j] != cls[j - 1]) pos = atomicAdd(&cnt[cls[j]], run[j]);
         else pos++;
         rk[j] = pos;
-        const int32_t L = Ls[j];
-        if (pos < (uint32_t)kOrderBlock && L >= 2 * kSegMin && L <= (int32_t)TOPK_L_MAX &&
-            row_sampled(a, i0 + j, L)) {
+        if (pos < (uint32_t)kOrderBlock) {
+            rrow[pos] = (uint32_t)(i0 + j);
+            rlen[pos] = Ls[j];
+        }
+    }
+    __syncthreads();
+    {
+        // thread tid: the segments of rank tid
+        const int32_t L = rlen[tid];
+        uint32_t P = 1;
+        if (L >= 2 * kSegMin && L <= (int32_t)TOPK_L_MAX && row_sampled(a, (int)rrow[tid], L)) {
             // ceil(L / S) from a single-precision quotient (off by at most
             // one: L / S < 2^18) and one exact integer correction
             uint32_t q = (uint32_t)ceilf((float)L * rS);
             if ((uint64_t)q * S < (uint64_t)L) q++;
             else if (q > 1u && (uint64_t)(q - 1u) * S >= (uint64_t)L) q--;
-            const uint32_t P = min(min((uint32_t)kMaxSplit, (uint32_t)L / (uint32_t)kSegMin), q);
-            rinfo[pos] = P - 1u;
+            P = min(min((uint32_t)kMaxSplit, (uint32_t)L / (uint32_t)kSegMin), q);
         }
+        rinfo[tid] = P - 1u;
     }
-    __syncthreads();
     {
         // rank tid: extra segments E and split rows Ns up to and including it
         // (sums of at most 63 x 1024 and 1024, packed in one word)
