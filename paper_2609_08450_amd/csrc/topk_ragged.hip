@@ -74,6 +74,11 @@ constexpr size_t kRowBlockBytes = kRowStateBytes + kViewHistBytes + 2 * kFront *
 // merged): one workgroup gathering them all is bound by its cache-line
 // fills (one 128-byte line per 4-byte sample).
 constexpr int64_t kCoopView = 4096;
+// The same for rows the item table cuts: their segments start among a whole
+// call's first loads, where segment 0 alone took 15-20 us to gather a view of
+// 1000-2000 samples (edge mix 76.9 -> 74.8 us per call from 1024; from 512
+// 75.7, from 2048 unchanged).
+constexpr int64_t kCoopViewTable = 1024;
 // Most segments a row may have for its segments to publish per wave.
 constexpr int64_t kWavePublishMaxSegs = 16;
 // Calls with more rows than can be resident run their rows longest first: a
@@ -2426,7 +2431,7 @@ topk_ragged_kernel(KArgs a) {
         // chunk in flight.  A large view of a split row is shared instead:
         // each segment reads the part inside its own range (after the plan).
         float xs[kP1];
-        const bool big_view = nv >= kCoopView && (a.pmax > 1 || Pe > 1);
+        const bool big_view = (nv >= kCoopView && a.pmax > 1) || (nv >= kCoopViewTable && Pe > 1);
         if (p == 0 && !big_view) phase1_issue(a, r, row, L, xs);
         // Segments: segment_plan when every row may be split, else the item
         // table's count.
