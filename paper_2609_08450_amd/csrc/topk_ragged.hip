@@ -2021,10 +2021,12 @@ __device__ __forceinline__ void reset_row_state(RowState *rs, bool x = true) {
 //
 // Exact coarse recovery (eq:method:exact-init) of a split row whose
 // candidates overflowed, spread over its segments.  Every segment with an
-// overflowed region has added the coarse histogram of its range into the
-// row's histogram; the finisher adds the other segments' stored candidates
-// (all of their elements with c <= tau1), which makes the histogram exact in
-// bins 0..tau1, where tau_star lies when C(tau1) >= K.  It publishes
+// overflowed region has added the coarse histogram of its range, exact in
+// bins 0..tau1 (its stored entries and the hits Phase 2 counted past its
+// region), into the row's histogram; the finisher adds the other segments'
+// stored candidates (all of their elements with c <= tau1), which makes the
+// histogram the row's own in bins 0..tau1, where tau_star lies when
+// C(tau1) >= K.  It publishes
 // tau_star, and each segment then classifies its own range (the finisher the
 // stored candidates): c < tau_star into the row's output (E0), c == tau_star
 // into the candidate buffer (Q0), at slots reserved with one atomic per
@@ -2059,9 +2061,9 @@ __device__ __forceinline__ void hist_lt_eq(Smem &sm, const uint32_t *h, uint32_t
 // global memory.  sm.opos and sm.cnt must be zero before a preceding
 // barrier.  Ends with a barrier.
 __device__ __forceinline__ void classify_range(const KArgs a, Smem &sm, int r, int64_t off,
-                                            int32_t beg, int32_t end, uint32_t key_lo,
-                                            uint32_t key_hi, uint32_t n_lt, uint32_t n_eq,
-                                            uint32_t glt, uint32_t geq, uint64_t *gc) {
+                                               int32_t beg, int32_t end, uint32_t key_lo,
+                                               uint32_t key_hi, uint32_t n_lt, uint32_t n_eq,
+                                               uint32_t glt, uint32_t geq, uint64_t *gc) {
     const int tid = threadIdx.x;
     const int lane = lane_id();
     const bool stage = n_lt + n_eq <= (uint32_t)kFront;
@@ -2069,9 +2071,8 @@ __device__ __forceinline__ void classify_range(const KArgs a, Smem &sm, int r, i
     int32_t *oi = a.out_idx + (int64_t)r * a.K;
     float *ov = a.out_val + (int64_t)r * a.K;
     static_assert(kVec * 4 <= 16 && kWaves * 64 * 16 < 65536, "packed counts");
-    stream_row<false>(a.scores, off, beg, end, [&](const f4 *x, const int32_t *i0,
-                                                            int32_t lo, int32_t hi, bool edge,
-                                                            int32_t mv) {
+    stream_row<false>(a.scores, off, beg, end, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                                   int32_t hi, bool edge, int32_t mv) {
         uint32_t mlt = 0, meq = 0;
 #pragma unroll
         for (int m = 0; m < kVec; m++) if (m < mv) {
