@@ -621,6 +621,42 @@ def test_segments_that_stop_waiting_build_the_view(topk):
     assert st["wait_fallback"] > 0
 
 
+def test_item_table_caps_a_row_at_64_segments(topk):
+    """A call of 600 rows, one of 8M elements (an eighth of the call's
+    length and more), two of 2M and short ones: the longest row gets the cap
+    of 64 segments (its own ceil(L / S) is larger), the 2M rows what the
+    rule gives, and every selection and trace still matches the oracle.  (The
+    extra-item budget of 2 x CUs cannot bind: the cut rows' extra items sum to
+    at most sum(L) / S <= 2 x CUs.)"""
+    import torch
+
+    rng = np.random.default_rng(59)
+    n = 600
+    lens = rng.integers(1000, 9000, n).astype(np.int32)
+    big = rng.choice(n, 3, replace=False)
+    lens[big[0]] = 8_000_000
+    lens[big[1:]] = 2_000_000
+    rows = [W.decode_mixture_row(rng, int(L)).astype(np.float32) for L in lens]
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload("segment cap", np.concatenate(rows), offs, lens, 2048, "")
+    gt, st = parity(topk, wl)
+    say("routes", st)
+    s, o, l = device_arrays(wl)
+    ws = topk.alloc_workspace(n, wl.K)
+    run_hip(s, o, l, wl.K, trace=False, ws=ws)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    extra = min(2 * cus, 1024)
+    tab = ws[1024:1024 + 16 * (n + extra)].cpu().numpy().view(np.uint32).reshape(-1, 4)
+    tab = tab.astype(np.int64)
+    first = ((tab[:, 0] >> 31) == 0) & (((tab[:, 0] >> 14) & 63) == 0)
+    seg = dict(zip((tab[first, 0] & 0x3FFF).tolist(), (((tab[first, 0] >> 20) & 63) + 1).tolist()))
+    S = max(8192, -(-int(lens.astype(np.int64).sum()) // (2 * cus)))
+    say("segments", seg[int(big[0])], seg[int(big[1])], seg[int(big[2])], "S", S)
+    assert seg[int(big[0])] == 64
+    for r in big[1:]:
+        assert seg[int(r)] == min(64, 2_000_000 // 8192, -(-2_000_000 // S))
+
+
 def _split_exact_workload():
     """600 rows: 60 long ones (150K-250K, cut into segments by the item table)
     among short ones.  Long row kinds by i % 4: 0 a decode row (primary); 1
