@@ -1831,35 +1831,12 @@ __device__ __forceinline__ void finish_row(const KArgs a, Smem &sm, int r, int64
     }
 }
 
-// Writes the K (index, FP32 bits) pairs staged in sm.ci/ck[0, K) to row
-// output out0: 16-byte stores when both output rows are 16-byte aligned,
-// else 4-byte ones (consecutive lanes, consecutive slots either way).
-__device__ __forceinline__ void store_staged(const KArgs a, const Smem &sm, int64_t out0) {
-    const uint32_t K = (uint32_t)a.K;
-    int32_t *oi = a.out_idx + out0;
-    float *ov = a.out_val + out0;
-    if (((reinterpret_cast<uintptr_t>(oi) | reinterpret_cast<uintptr_t>(ov)) & 15u) == 0 &&
-        (K & 3u) == 0) {
-        const uint4 *si = reinterpret_cast<const uint4 *>(sm.ci);
-        const uint4 *sk = reinterpret_cast<const uint4 *>(sm.ck);
-        for (uint32_t e = threadIdx.x; e < K / 4; e += kBlock) {
-            reinterpret_cast<uint4 *>(oi)[e] = si[e];
-            reinterpret_cast<uint4 *>(ov)[e] = sk[e];
-        }
-    } else {
-        for (uint32_t e = threadIdx.x; e < K; e += kBlock) {
-            oi[e] = (int32_t)sm.ci[e];
-            ov[e] = __builtin_bit_cast(float, sm.ck[e]);
-        }
-    }
-}
-
 // Finish of a row certified on the primary or band route, straight from its
 // candidates in registers (vi, vk: index and FP32 bits): one digit round over
 // the live key range [~amax, ~cut] (fine histogram plus 32-bin group sums,
-// two-level find), committed entries written out from registers in
-// consecutive slots of each wave, the boundary bin ranked when it holds at
-// most kSmall entries.  Slot (j, thread) holds a candidate iff j < ngroups
+// two-level find), committed entries stored from registers straight to
+// consecutive output slots of each wave, the boundary bin ranked (and stored)
+// when it holds at most kSmall entries.  Slot (j, thread) holds a candidate iff j < ngroups
 // (block-uniform) and j * unit + pos < lim: the merged array of a split row
 // has unit = kBlock, pos = thread, lim = count; the per-wave regions of a
 // single workgroup have unit = 64, pos = lane, lim = the wave's count.
@@ -1942,8 +1919,8 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
     PHASE_MARK(a, 11);
     const int64_t out0 = (int64_t)r * a.K;
     uint64_t *zs = reinterpret_cast<uint64_t *>(sm.hist2);
-    // committed entries are staged in sm.ci/ck[0, K) (free in this path: the
-    // candidates are in registers; K <= n_live <= cap < kFront)
+    // committed entries go straight to their output slots (slot order is
+    // free: the outputs are a set)
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
         if ((uint32_t)j >= ngroups) continue;
@@ -1952,8 +1929,7 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
         if (commit) {
             const uint32_t pos = cbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
                                                __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u));
-            sm.ci[pos] = vi[j];
-            sm.ck[pos] = vk[j];
+            put_out(a, out0, pos, vi[j], vk[j]);
         }
         cbase += (uint32_t)__popcll(mc);
         const bool keep = !take_all && tl[j] - cb <= kw;
@@ -1975,14 +1951,9 @@ __device__ __forceinline__ bool finish_fast(const KArgs a, Smem &sm, int r, int6
     if (!take_all) {
         __syncthreads();
         rank_small_to(zs, f.eq, need, f.below, [&](uint32_t pos, uint32_t idx, uint32_t bits) {
-            sm.ci[pos] = idx;
-            sm.ck[pos] = bits;
+            put_out(a, out0, pos, idx, bits);
         });
     }
-    // The K outputs were staged in LDS (slot order is free): write them out
-    // with few, wide stores.
-    __syncthreads();
-    store_staged(a, sm, out0);
     PHASE_MARK(a, 13);
     if (tid == 0) {
         atomicAdd(&a.hdr->stats[route], 1u);
