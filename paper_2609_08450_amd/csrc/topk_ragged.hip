@@ -2309,11 +2309,16 @@ topk_ragged_kernel(KArgs a) {
     // (used only when rows may be split).  (all loaded unconditionally and
     // selected afterwards: a branch here would cost a second round trip)
     constexpr bool ordered = kOrdered;
+    // rows split by plan (never in an item-table call)
+    const bool plan_split = !kOrdered && a.pmax > 1;
     const int ri = item - pi * a.n_rows;
+    // (an item-table call never splits by plan and takes the row from its
+    // entry: it loads no length or offset, and its wait holds no vector load,
+    // which under load would queue behind the other workgroup's stream)
     const uint4 e = *(ordered ? a.order + item : reinterpret_cast<const uint4 *>(a.hdr));
-    const int32_t len_i = a.lens[ri];
-    const int64_t off_i = a.offs[ri];
-    const int32_t len0_raw = a.lens[min(tid, a.n_rows - 1)];
+    const int32_t len_i = ordered ? 0 : a.lens[ri];
+    const int64_t off_i = ordered ? 0 : a.offs[ri];
+    const int32_t len0_raw = ordered ? 0 : a.lens[min(tid, a.n_rows - 1)];
     const uint4 hw = *reinterpret_cast<const uint4 *>(a.hdr); // magic, split_rows, max_rows
     // (keeps the compiler from sinking each load to its first use, which
     // would make them several round trips instead of one)
@@ -2336,7 +2341,7 @@ topk_ragged_kernel(KArgs a) {
 
     // Workspace check: a split plan needs per-row state for every row.
     const bool ws_bad = (hw.x != kMagic) | ((uint32_t)a.n_rows > hw.z) |
-                        ((a.pmax > 1) & ((uint32_t)a.n_rows > hw.y));
+                        (plan_split & ((uint32_t)a.n_rows > hw.y));
     if (ws_bad) {
         if (p == 0) {
             write_error_row(a, r);
@@ -2403,12 +2408,12 @@ topk_ragged_kernel(KArgs a) {
         // chunk in flight.  A large view of a split row is shared instead:
         // each segment reads the part inside its own range (after the plan).
         float xs[kP1];
-        const bool big_view = (nv >= kCoopView && a.pmax > 1) || (nv >= kCoopViewTable && Pe > 1);
+        const bool big_view = (nv >= kCoopView && plan_split) || (nv >= kCoopViewTable && Pe > 1);
         if (p == 0 && !big_view) phase1_issue(a, r, row, L, xs);
         // Segments: segment_plan when every row may be split, else the item
         // table's count.
         int64_t P = 1, seg = L;
-        if (a.pmax > 1) {
+        if (plan_split) {
             segment_plan(a, block_total_length(a, sm.lsum, tid < a.n_rows ? len0_raw : 0), L, P, seg);
         } else if (Pe > 1) {
             P = Pe;
@@ -2445,7 +2450,7 @@ topk_ragged_kernel(KArgs a) {
                 have = coop_view_finish(a, sm, r, row, k0, k1, xs, rs, vh, P);
             } else if (p == 0) {
                 // (a split plan's length sum ended with a barrier)
-                phase1_finish(a, sm, r, row, L, xs, split ? &rs->taus : nullptr, a.pmax > 1);
+                phase1_finish(a, sm, r, row, L, xs, split ? &rs->taus : nullptr, plan_split);
                 have = true;
             }
             if (!have) {
