@@ -2342,7 +2342,7 @@ topk_ragged_kernel(KArgs a) {
     // Workspace check: a split plan needs per-row state for every row.
     const bool ws_bad = (hw.x != kMagic) | ((uint32_t)a.n_rows > hw.z) |
                         (plan_split & ((uint32_t)a.n_rows > hw.y));
-    if (ws_bad) {
+    if (__builtin_expect(ws_bad, 0)) {
         if (p == 0) {
             write_error_row(a, r);
             if (tid == 0 && r == 0) atomicAdd(&a.hdr->stats[kStatErrors], 1u);
@@ -2351,7 +2351,7 @@ topk_ragged_kernel(KArgs a) {
     }
     // A row longer than TOPK_L_MAX would overflow the 32-bit byte offsets of
     // its vectors: it is not selected, and counted as an error.
-    if (L > (int64_t)TOPK_L_MAX) {
+    if (__builtin_expect(L > (int64_t)TOPK_L_MAX, 0)) {
         if (p == 0) {
             write_error_row(a, r);
             if (tid == 0) atomicAdd(&a.hdr->stats[kStatErrors], 1u);
@@ -2463,7 +2463,7 @@ topk_ragged_kernel(KArgs a) {
                         __builtin_amdgcn_s_sleep(1);
                     }
                     PHASE_MARK(a, 20);
-                    if (v & 0x80000000u) {
+                    if (__builtin_expect((v & 0x80000000u) != 0, 1)) {
                         sm.flag = 1u;
                         sm.tau0 = v & 0xFFFFu;
                         sm.tau1 = (v >> 16) & 0x7FFFu;
@@ -2475,7 +2475,7 @@ topk_ragged_kernel(KArgs a) {
                     }
                 }
                 __syncthreads();
-                if (sm.flag == 0u) {
+                if (__builtin_expect(sm.flag == 0u, 0)) {
                     // the whole view, on its own (sm.hist may hold this
                     // segment's part of a shared view)
                     clear_hist(sm);
@@ -2505,7 +2505,7 @@ topk_ragged_kernel(KArgs a) {
         uint32_t wcnt = 0, dst = 0; // this wave's stored entries, and their first slot
         if (wave_publish) {
             const uint32_t cur_w = sm.wcnt[w8]; // this wave's own count
-            if (cur_w <= (uint32_t)kWaveCap) {
+            if (__builtin_expect(cur_w <= (uint32_t)kWaveCap, 1)) {
                 wcnt = cur_w;
                 uint32_t wres = 0;
                 if (lane == 0 && wcnt)
