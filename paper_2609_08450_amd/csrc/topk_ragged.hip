@@ -2447,6 +2447,9 @@ topk_ragged_kernel(KArgs a) {
         phase2_collect<kOrdered>(sm, a.scores, off, beg, end, [&]() {
             bool have = false; // endpoints in sm
             if (coop) {
+                // (orders the clear of sm.hist before the additions: only a
+                // split plan's length sum has a barrier after it)
+                if (!plan_split) __syncthreads();
                 have = coop_view_finish(a, sm, r, row, k0, k1, xs, rs, vh, P);
             } else if (p == 0) {
                 // (a split plan's length sum ended with a barrier)
