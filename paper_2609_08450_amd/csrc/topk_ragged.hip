@@ -2453,7 +2453,13 @@ topk_ragged_kernel(KArgs a) {
                 have = coop_view_finish(a, sm, r, row, k0, k1, xs, rs, vh, P);
             } else if (p == 0) {
                 // (a split plan's length sum ended with a barrier)
+                // (in an item-table call the waves that find the boundaries,
+                // and below those of a finisher, issue ahead of the CU's
+                // streaming waves: the edge mix 74.8 -> 73.7 us; in the
+                // other instance it made the decode batch slower)
+                if constexpr (kOrdered) __builtin_amdgcn_s_setprio(2);
                 phase1_finish(a, sm, r, row, L, xs, split ? &rs->taus : nullptr, plan_split);
+                if constexpr (kOrdered) __builtin_amdgcn_s_setprio(0);
                 have = true;
             }
             if (!have) {
@@ -2698,6 +2704,7 @@ topk_ragged_kernel(KArgs a) {
             }
 
             if (!redo) {
+            if constexpr (kOrdered) __builtin_amdgcn_s_setprio(2); // (see the boundaries)
             // Finisher (its sm.cut0, cut1, tau0, tau1 are the row's endpoints).
             // The counts and the slot groups that hold candidates are loaded
             // in one round trip (slots past the stored count in the last
