@@ -1,0 +1,78 @@
+"""Seeded mixed calls: every row kind the selector routes differently, in one
+call, at random lengths, buffer positions and alignments, for both kernel
+instances (calls of at most and of more than 2 x CUs rows) and several K;
+selections and route traces compared with the oracle, bit-exact."""
+import numpy as np
+import pytest
+
+from paper_2609_08450_amd import workloads as W
+from tests.test_gpu_parity import parity, say, topk  # noqa: F401  (topk: the fixture)
+
+pytestmark = pytest.mark.gpu
+
+KINDS = ("decode", "codebook", "view low", "view high", "minus inf", "hot block",
+         "copies of one", "constant")
+
+
+def mixed_row(rng, kind, L, phase):
+    """A row of length L of the given kind (phase: the row's view phase at
+    stride 128, which the strided kinds target)."""
+    if L == 0:
+        return np.zeros(0, np.float32)
+    x = W.decode_mixture_row(rng, L).astype(np.float32)
+    if kind == "codebook":
+        book = np.unique(rng.standard_normal(4096).astype(np.float32))[:int(rng.integers(2, 300))]
+        x = book[rng.integers(0, book.size, L)]
+    elif kind == "view low":
+        x[phase::128] = rng.normal(-2.0, 1.0, x[phase::128].size).astype(np.float32)
+    elif kind == "view high":
+        x[phase::128] = rng.normal(3.0, 0.5, x[phase::128].size).astype(np.float32)
+    elif kind == "minus inf":
+        x[rng.random(L) < rng.uniform(0.2, 0.999)] = -np.inf
+    elif kind == "hot block":
+        a = int(rng.integers(0, L))
+        b = min(L, a + int(rng.integers(1, 6000)))
+        x[a:b] = rng.normal(4.0, 0.1, b - a).astype(np.float32)
+    elif kind == "copies of one":
+        x = rng.normal(-3.0, 0.5, L).astype(np.float32)
+        x[rng.choice(L, min(L, 10000), replace=False)] = 1.0
+    elif kind == "constant":
+        x[:] = np.float32(rng.choice([0.0, -0.0, 1.5, -np.inf]))
+    return x.astype(np.float32, copy=False)
+
+
+def mixed_workload(seed):
+    rng = np.random.default_rng(9000 + seed)
+    n = int(rng.choice([40, 300, 700, 1200]))
+    K = int(rng.choice([2048, 2048, 256, 1024, 4096]))
+    u = rng.random(n)
+    lens = np.floor(np.exp(np.log(1.0) + u * np.log(300000.0))).astype(np.int64) - 1
+    lens[rng.random(n) < 0.05] = 0
+    lens[rng.random(n) < 0.05] = K
+    # a few long rows, so that both the plan and the item table cut some
+    longs = rng.choice(n, max(1, n // 40), replace=False)
+    lens[longs] = rng.integers(150000, 600000, longs.size)
+    lens = np.minimum(lens, 600000)
+    parts, offs, pos = [], np.zeros(n, np.int64), 0
+    for r in rng.permutation(n):               # buffer order differs from row order
+        gap = int(rng.integers(0, 9))           # any 4-byte alignment
+        parts.append(np.zeros(gap, np.float32))
+        pos += gap
+        kind = KINDS[int(rng.integers(0, len(KINDS)))]
+        phase = int(format(int(r) % 128, "07b")[::-1], 2)
+        x = mixed_row(rng, kind, int(lens[r]), phase)
+        parts.append(x)
+        offs[r] = pos
+        pos += x.size
+    buf = np.concatenate(parts + [np.zeros(8, np.float32)])
+    return W.Workload(f"mixed seed {seed}", buf, offs, lens.astype(np.int32), K,
+                      f"{n} mixed rows, K={K}")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_mixed_call(topk, seed):
+    wl = mixed_workload(seed)
+    say("mixed", seed, "rows", wl.n_rows, "K", wl.K, "sum L", wl.total_len)
+    gt, st = parity(topk, wl, where=f"mixed seed {seed}", per_k=True)
+    say("routes", st)
+    assert st["errors"] == 0
