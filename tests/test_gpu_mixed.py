@@ -2,6 +2,8 @@
 call, at random lengths, buffer positions and alignments, for both kernel
 instances (calls of at most and of more than 2 x CUs rows) and several K;
 selections and route traces compared with the oracle, bit-exact."""
+import os
+
 import numpy as np
 import pytest
 
@@ -69,7 +71,13 @@ def mixed_workload(seed):
                       f"{n} mixed rows, K={K}")
 
 
-@pytest.mark.parametrize("seed", range(6))
+def _seeds():
+    """Seeds 0-5, or the range TOPK_MIXED_SEEDS=a:b (a wider sweep)."""
+    a, b = os.environ.get("TOPK_MIXED_SEEDS", "0:6").split(":")
+    return range(int(a), int(b))
+
+
+@pytest.mark.parametrize("seed", _seeds())
 def test_mixed_call(topk, seed):
     wl = mixed_workload(seed)
     say("mixed", seed, "rows", wl.n_rows, "K", wl.K, "sum L", wl.total_len)
