@@ -84,3 +84,19 @@ def test_mixed_call(topk, seed):
     gt, st = parity(topk, wl, where=f"mixed seed {seed}", per_k=True)
     say("routes", st)
     assert st["errors"] == 0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_mixed_call_one_poll(topk, seed):
+    """The same calls with one poll allowed for every bounded wait, so that
+    segments stop waiting for the boundaries or the route word and take their
+    fallbacks (building the view themselves, leaving their range to the last
+    arrival): the same selections and traces."""
+    wl = mixed_workload(seed)
+    topk.debug_set_spin_limit(1)
+    try:
+        gt, st = parity(topk, wl, where=f"mixed seed {seed}, one poll", per_k=True)
+    finally:
+        topk.debug_set_spin_limit(0)
+    say("routes", st)
+    assert st["errors"] == 0
