@@ -45,6 +45,31 @@ def test_noalloc_matches_topk_ragged():
     _both(topk, W.tiny())
 
 
+def test_noalloc_mixed_calls_in_a_row():
+    """Seeded mixed calls (every row kind, 40 to 1200 rows, K from 256 to
+    4096) one after another through the allocation-free entry point, each
+    against the oracle: the state the kernels leave in the shared array
+    serves the next call whatever its size."""
+    import torch
+
+    import oracle
+    from paper_2609_08450_amd import topk
+    from tests.test_gpu_mixed import mixed_workload
+
+    for seed in range(6):
+        wl = mixed_workload(seed)
+        n, K = wl.n_rows, wl.K
+        print("[case] noalloc mixed seed", seed, "rows", n, "K", K, flush=True)
+        s, o, l = device_arrays(wl)
+        gi = torch.full((n, K), -9, dtype=torch.int32, device="cuda")
+        gv = torch.full((n, K), 9.0, dtype=torch.float32, device="cuda")
+        topk.topk_ragged_noalloc(s, o, l, n, K, gi, gv)
+        torch.cuda.synchronize()
+        oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, K)
+        assert_same_selection(gi.cpu().numpy(), gv.cpu().numpy(), oi, ov,
+                              where=f"noalloc mixed seed {seed}")
+
+
 def test_noalloc_rejects_too_many_rows():
     import torch
 
