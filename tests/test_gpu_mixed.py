@@ -100,3 +100,51 @@ def test_mixed_call_one_poll(topk, seed):
         topk.debug_set_spin_limit(0)
     say("routes", st)
     assert st["errors"] == 0
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_mixed_call_graph_replays(topk, seed):
+    """A mixed call captured in a HIP graph and replayed three times, with an
+    eager call of another mix on the same workspace between replays: every
+    replay and every eager call equal the oracle (the kernels leave the
+    workspace's state as they found it, whatever routes a call took)."""
+    import torch
+
+    import oracle
+    from tests.gpu_util import assert_same_selection, device_arrays
+
+    wl, other = mixed_workload(seed), mixed_workload(seed + 1000)
+    n, K, n2, K2 = wl.n_rows, wl.K, other.n_rows, other.K
+    say("graph", seed, "rows", n, "K", K, "between", n2, K2)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        s, o, l = device_arrays(wl)
+        s2, o2, l2 = device_arrays(other)
+        ws = topk.alloc_workspace(max(n, n2), max(K, K2), torch.device("cuda", 0), stream)
+        gi = torch.full((n, K), -9, dtype=torch.int32, device="cuda")
+        gv = torch.full((n, K), 9.0, dtype=torch.float32, device="cuda")
+        ei = torch.empty((n2, K2), dtype=torch.int32, device="cuda")
+        ev = torch.empty((n2, K2), dtype=torch.float32, device="cuda")
+    stream.synchronize()
+    topk.topk_ragged(s, o, l, n, K, gi, gv, ws, stream)
+    stream.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        topk.topk_ragged(s, o, l, n, K, gi, gv, ws, torch.cuda.current_stream())
+    stream.synchronize()
+    oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, K)
+    oi2, ov2 = oracle.topk_ragged(other.scores, other.row_offsets, other.row_lengths, K2)
+    for rep in range(3):
+        with torch.cuda.stream(stream):
+            gi.fill_(-9)
+            gv.fill_(9.0)
+        stream.synchronize()
+        g.replay()
+        stream.synchronize()
+        assert_same_selection(gi.cpu().numpy(), gv.cpu().numpy(), oi, ov,
+                              where=f"graph seed {seed} replay {rep}")
+        topk.topk_ragged(s2, o2, l2, n2, K2, ei, ev, ws, stream)
+        stream.synchronize()
+        assert_same_selection(ei.cpu().numpy(), ev.cpu().numpy(), oi2, ov2,
+                              where=f"eager mix between replays {rep}")
+    del g
