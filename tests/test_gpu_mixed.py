@@ -148,3 +148,16 @@ def test_mixed_call_graph_replays(topk, seed):
         assert_same_selection(ei.cpu().numpy(), ev.cpu().numpy(), oi2, ov2,
                               where=f"eager mix between replays {rep}")
     del g
+
+
+@pytest.mark.parametrize("K", [1, 3, 7168, 16384])
+def test_mixed_call_extreme_k(topk, K):
+    """Mixed rows at the ends of the K range (a few outputs per row; a K at and
+    past the LDS frontier, 16384 at most 300 rows): selections and traces."""
+    wl = mixed_workload(K % 97)
+    n = wl.n_rows if K <= 8192 else min(wl.n_rows, 300)
+    wl = W.Workload(wl.name, wl.scores, wl.row_offsets[:n].copy(), wl.row_lengths[:n].copy(),
+                    K, "")
+    gt, st = parity(topk, wl, where=f"mixed rows, K {K}", per_k=True)
+    say("routes", st)
+    assert st["errors"] == 0
