@@ -84,7 +84,8 @@ typedef struct topk_ragged_policy {
     int32_t s_log2;     /* view stride s = 2^s_log2, 0 <= s_log2 <= 12 */
     int32_t rho_num;    /* K~  = ceil(rho_num  K / rho_den)  (as sample rank) */
     int32_t rho_den;
-    int32_t rho1_num;   /* K~1 = ceil(rho1_num K / rho1_den) (nested target) */
+    int32_t rho1_num;   /* K~1 = ceil(rho1_num K / rho1_den) (nested target;
+                           raised to K~ when below it) */
     int32_t rho1_den;
     int32_t l_samp_min; /* rows shorter than this take the exact route; a
                            negative value -m means m * K */

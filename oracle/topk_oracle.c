@@ -235,9 +235,10 @@ int oracle_topk_ragged(const float *scores, const int64_t *row_offsets,
 /* ------------------------------------------------------- route model ----- */
 
 /* Policy of the sampled pipeline.  rho = rho_num / rho_den is the retention
- * margin (K~ = rho K), rho1 the nested secondary target (K~1 = rho1 K); s is
- * the view stride; rows with L < l_samp_min or a view smaller than q1 take the
- * exact route; cap is the frontier capacity: a candidate set larger than cap
+ * margin (K~ = rho K), rho1 the nested secondary target (K~1 = rho1 K, raised
+ * to K~ when below it); s is the view stride; rows with L < l_samp_min or a
+ * view smaller than q1 take the exact route; cap is the frontier capacity: a
+ * candidate set larger than cap
  * is not materialised (sampled rows then take exact coarse recovery; an exact
  * boundary bin larger than cap is resolved by re-reading the row). */
 typedef struct {
@@ -345,7 +346,12 @@ int oracle_route_model(const float *scores, const int64_t *row_offsets,
 #endif
     const int32_t s = pol->s;
     const int32_t q0 = oracle_sample_rank(K, pol->rho_num, pol->rho_den, s);
-    const int32_t q1 = oracle_sample_rank(K, pol->rho1_num, pol->rho1_den, s);
+    /* The nested target is never below the primary one (Section 4.3: tau1 is
+     * the looser, nested boundary, K~1 >= K~).  A policy that sets it lower
+     * gets K~1 = K~, so a sampled row's view holds both ranks and tau1 = tau0. */
+    int32_t q1 = oracle_sample_rank(K, pol->rho1_num, pol->rho1_den, s);
+    if (q1 < q0)
+        q1 = q0;
     int bad = 0;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
     for (int32_t r = 0; r < n_rows; r++) {

@@ -154,6 +154,7 @@ def _mixed(K=2048):
     ("tiny cap", {"cap": 600}),
     ("underfill", {"rho_num": 1, "rho_den": 2, "rho1_num": 3, "rho1_den": 4}),
     ("no band margin", {"rho_num": 1, "rho_den": 1, "rho1_num": 1, "rho1_den": 1}),
+    ("nested target below", {"rho_num": 5, "rho_den": 2, "rho1_num": 5, "rho1_den": 4}),
     ("stride 64", {"s_log2": 6, "l_samp_min": 4096}),
     ("stride 1", {"s_log2": 0, "l_samp_min": 4096}),
     ("stride 4096", {"s_log2": 12, "l_samp_min": 0}),

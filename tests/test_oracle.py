@@ -247,7 +247,7 @@ def _route_checks(wl, K, pol, rows=None):
     pi, pv = oracle.topk_ragged(sub.scores, sub.row_offsets, sub.row_lengths, K)
     s = pol.s
     q0 = math.ceil(pol.rho_num * K / (pol.rho_den * s))
-    q1 = math.ceil(pol.rho1_num * K / (pol.rho1_den * s))
+    q1 = max(q0, math.ceil(pol.rho1_num * K / (pol.rho1_den * s)))  # K~1 >= K~
     for j, r in enumerate(rows):
         x = sub.row(j)
         L = x.size
@@ -321,3 +321,30 @@ def test_route_model_policies(s, cap, lmin):
     offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
     wl = W.Workload("policies", buf, offs, lens, 1000, "")
     _route_checks(wl, 1000, oracle.default_policy(s=s, cap=cap, l_samp_min=lmin))
+
+
+def test_route_model_nested_target_below_the_primary():
+    """A policy whose nested target K~1 is below K~ (rho1 < rho) gets
+    K~1 = K~: the nested boundary is never tighter than the primary one, so a
+    row is sampled only when its view holds the primary rank, and tau1 =
+    tau0.  Rows whose view size falls between the two ranks take the exact
+    route.  (K = 1000, s = 4: q0 = 1250, the unraised q1 would be 375.)"""
+    rng = np.random.default_rng(61)
+    rows = []
+    for L in (1600, 3000, 4999, 5000, 5001, 5003, 9000):
+        x = rng.standard_normal(L).astype(np.float32)
+        rows.append(x)
+        rows.append(np.round(x * 4).astype(np.float32))
+    buf = np.concatenate(rows)
+    lens = np.array([r.size for r in rows], np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload("nested below primary", buf, offs, lens, 1000, "")
+    pol = oracle.default_policy(s=4, rho_num=5, rho_den=1, rho1_num=3, rho1_den=2, l_samp_min=0)
+    tr = _route_checks(wl, 1000, pol)
+    q0 = math.ceil(5 * 1000 / 4)
+    for j in range(wl.n_rows):
+        if tr[j][2] >= 0:
+            assert tr[j][1] >= q0 and tr[j][3] == tr[j][2]
+        elif lens[j] > 1000:
+            assert tr[j][1] < q0 and tr[j][0] == oracle.ROUTE_EXACT_UNSAMPLED
+    assert np.any(tr[:, 2] >= 0) and np.any((tr[:, 2] < 0) & (lens > 1000))
