@@ -1,7 +1,8 @@
-"""Seeded mixed calls: every row kind the selector routes differently, in one
-call, at random lengths, buffer positions and alignments, for both kernel
-instances (calls of at most and of more than 2 x CUs rows) and several K;
-selections and route traces compared with the oracle, bit-exact."""
+"""Seeded mixed calls: every row kind the selector routes differently, and
+special FP32 values, in one call, at random lengths, buffer positions and
+alignments, for both kernel instances (calls of at most and of more than
+2 x CUs rows) and several K; selections and route traces compared with the
+oracle, bit-exact."""
 import os
 
 import numpy as np
@@ -13,7 +14,13 @@ from tests.test_gpu_parity import parity, say, topk  # noqa: F401  (topk: the fi
 pytestmark = pytest.mark.gpu
 
 KINDS = ("decode", "codebook", "view low", "view high", "minus inf", "hot block",
-         "copies of one", "constant")
+         "copies of one", "constant", "specials")
+
+# +-inf, +-0, the largest finite values, the smallest normals, subnormals, and
+# values around FP16's largest finite (65504) and smallest subnormal (2^-24)
+SPECIALS = np.array([np.inf, -np.inf, 0.0, -0.0, 3.4028235e38, -3.4028235e38,
+                     1.1754944e-38, -1.1754944e-38, 1e-45, -1e-45, 3e-39, -3e-39,
+                     65504.0, 65520.0, -65520.0, 5.96e-8, 2.98e-8, -2.98e-8], np.float32)
 
 
 def mixed_row(rng, kind, L, phase):
@@ -40,6 +47,9 @@ def mixed_row(rng, kind, L, phase):
         x[rng.choice(L, min(L, 10000), replace=False)] = 1.0
     elif kind == "constant":
         x[:] = np.float32(rng.choice([0.0, -0.0, 1.5, -np.inf]))
+    elif kind == "specials":
+        m = rng.random(L) < rng.uniform(0.01, 0.9)
+        x[m] = SPECIALS[rng.integers(0, SPECIALS.size, int(m.sum()))]
     return x.astype(np.float32, copy=False)
 
 
@@ -159,5 +169,24 @@ def test_mixed_call_extreme_k(topk, K):
     wl = W.Workload(wl.name, wl.scores, wl.row_offsets[:n].copy(), wl.row_lengths[:n].copy(),
                     K, "")
     gt, st = parity(topk, wl, where=f"mixed rows, K {K}", per_k=True)
+    say("routes", st)
+    assert st["errors"] == 0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_mixed_call_random_policy(topk, seed):
+    """Mixed calls under a random valid policy (stride 1 to 4096, any margins,
+    including a nested target below the primary one, any sampling floor and
+    frontier capacity): selections and traces."""
+    rng = np.random.default_rng(7000 + seed)
+    wl = mixed_workload(seed)
+    pol = topk.default_policy()
+    pol.s_log2 = int(rng.integers(0, 13))
+    pol.rho_num, pol.rho_den = int(rng.integers(1, 9)), int(rng.integers(1, 5))
+    pol.rho1_num, pol.rho1_den = int(rng.integers(1, 9)), int(rng.integers(1, 5))
+    pol.l_samp_min = int(rng.choice([0, 1024, 8192, 65536, -1, -4, -16]))
+    pol.cap = int(rng.choice([1, 100, 2048, 4095, 6144]))
+    say("policy", pol.as_dict())
+    gt, st = parity(topk, wl, policy=pol, where=f"mixed seed {seed}, random policy")
     say("routes", st)
     assert st["errors"] == 0
