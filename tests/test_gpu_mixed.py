@@ -190,3 +190,47 @@ def test_mixed_call_random_policy(topk, seed):
     gt, st = parity(topk, wl, policy=pol, where=f"mixed seed {seed}, random policy")
     say("routes", st)
     assert st["errors"] == 0
+
+
+def shaped_workload(seed, n):
+    """n rows of random kinds and lengths (about 15 M elements in all; up to
+    700K per row when n <= 64), some lengths negative (read as 0), some rows
+    overlapping earlier ones in the buffer."""
+    rng = np.random.default_rng(12000 + seed)
+    K = int(rng.choice([1, 16, 256, 2048, 4096]))
+    mean = max(64, 30_000_000 // max(n, 1) // 2)
+    lens = rng.integers(0, 2 * mean, n).astype(np.int64)
+    if n <= 64:
+        lens[:] = rng.integers(0, 700000, n)
+    lens[rng.random(n) < 0.03] = -int(rng.integers(1, 100))
+    pos, parts, offs = 0, [], np.zeros(n, np.int64)
+    for r in range(n):
+        L = max(int(lens[r]), 0)
+        if r > 0 and pos > 0 and rng.random() < 0.1:
+            offs[r] = int(rng.integers(0, pos))
+            need = offs[r] + L - pos
+            if need > 0:
+                parts.append(rng.standard_normal(need).astype(np.float32))
+                pos += need
+            continue
+        gap = int(rng.integers(0, 5))
+        parts.append(np.zeros(gap, np.float32))
+        pos += gap
+        x = mixed_row(rng, KINDS[int(rng.integers(0, len(KINDS)))], L,
+                      int(format(r % 128, "07b")[::-1], 2))
+        parts.append(x)
+        offs[r] = pos
+        pos += x.size
+    buf = np.concatenate(parts + [np.zeros(1, np.float32)]).astype(np.float32)
+    return W.Workload(f"shape n={n}", buf, offs, lens.astype(np.int32), K, "")
+
+
+@pytest.mark.parametrize("n", [1, 513, 16385])
+def test_call_shapes(topk, n):
+    """One row; one row past the split plan's limit (the item table); one row
+    past the item table's (index order), with negative lengths and rows that
+    overlap others in the buffer."""
+    wl = shaped_workload(n, n)
+    gt, st = parity(topk, wl, where=wl.name, per_k=True)
+    say("routes", st)
+    assert st["errors"] == 0
