@@ -170,7 +170,8 @@ int topk_ragged_workspace_init(void *workspace, size_t bytes, int32_t max_rows, 
  *   out_val      device, FP32 [n_rows x K], bit-exact copies of the scores.
  *   workspace    device, 256-byte aligned (as hipMalloc returns), initialised
  *                by topk_ragged_workspace_init with max_rows >= n_rows; not
- *                shared by concurrent calls.
+ *                shared by concurrent calls (calls with separate workspaces
+ *                may run concurrently, e.g. on different streams).
  * Row lengths and offsets stay on the device; the launch geometry depends
  * only on (n_rows, K, device).  A call of more than 2 x CUs and at most
  * 16384 rows enqueues a one-workgroup pre-pass before the main kernel: it

@@ -234,3 +234,34 @@ def test_call_shapes(topk, n):
     gt, st = parity(topk, wl, where=wl.name, per_k=True)
     say("routes", st)
     assert st["errors"] == 0
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_concurrent_calls_with_separate_workspaces(topk, seed):
+    """Two mixed calls on two streams, each with its own workspace, launched
+    back to back three times so that they overlap on the GPU: both equal the
+    oracle every time."""
+    import torch
+
+    import oracle
+    from tests.gpu_util import assert_same_selection, device_arrays
+
+    streams = (torch.cuda.Stream(), torch.cuda.Stream())
+    calls = []
+    for w, st in zip((mixed_workload(seed), mixed_workload(seed + 5000)), streams):
+        with torch.cuda.stream(st):
+            s, o, l = device_arrays(w)
+            ws = topk.alloc_workspace(w.n_rows, w.K, torch.device("cuda", 0), st)
+            gi = torch.full((w.n_rows, w.K), -9, dtype=torch.int32, device="cuda")
+            gv = torch.full((w.n_rows, w.K), 9.0, dtype=torch.float32, device="cuda")
+        ref = oracle.topk_ragged(w.scores, w.row_offsets, w.row_lengths, w.K)
+        calls.append((w, st, s, o, l, ws, gi, gv, ref))
+    torch.cuda.synchronize()
+    say("concurrent", [(c[0].n_rows, c[0].K) for c in calls])
+    for rep in range(3):
+        for w, st, s, o, l, ws, gi, gv, _ in calls:
+            topk.topk_ragged(s, o, l, w.n_rows, w.K, gi, gv, ws, st)
+        torch.cuda.synchronize()
+        for w, st, s, o, l, ws, gi, gv, (oi, ov) in calls:
+            assert_same_selection(gi.cpu().numpy(), gv.cpu().numpy(), oi, ov,
+                                  where=f"{w.name}, concurrent, rep {rep}")
