@@ -5,6 +5,8 @@ plain-definition oracle (bit-exact); per-row route traces are compared with
 the oracle's step-by-step model (integer-exact).  Every case prints its name
 before touching the GPU.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -14,6 +16,7 @@ from tests.gpu_util import assert_same_selection, device_arrays, oracle_policy_o
 from tests.invariants import check_row
 
 pytestmark = pytest.mark.gpu
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 @pytest.fixture(scope="module")
@@ -733,3 +736,37 @@ def test_read_ceiling_reads_every_score(topk, cfg):
         if x.size:
             want[r] = oracle.asc32(x.view(np.uint32)).max()
     assert np.array_equal(got, want)
+
+
+def test_rows_at_the_length_limit(topk):
+    """Rows of exactly TOPK_L_MAX elements (2^30 - 5), at an aligned offset and
+    at the worst misalignment (3 elements), whose Top-K is known by
+    construction: K distinct positive values planted among negative ones.
+    Both return exactly the planted (index, value) set.  A row one element
+    longer is rejected on the device: -1 / -inf and one error count."""
+    import re
+
+    import torch
+
+    text = open(os.path.join(ROOT, "include", "topk_ragged.h")).read()
+    lmax = int(re.search(r"#define TOPK_L_MAX (0x[0-9A-Fa-f]+)", text).group(1), 16)
+    K = 2048
+    say("rows of", lmax, "elements")
+    x = torch.rand(lmax + 4, device="cuda")
+    x.add_(1.0).neg_()                            # every value in (-2, -1]
+    rng = np.random.default_rng(71)
+    pos = np.sort(rng.choice(np.arange(3, lmax, dtype=np.int64), K, replace=False))
+    vals = (1.0 + rng.permutation(K) / 4096.0).astype(np.float32)
+    x[torch.from_numpy(pos).cuda()] = torch.from_numpy(vals).cuda()
+    offs = torch.tensor([0, 3, 0], dtype=torch.int64, device="cuda")
+    lens = torch.tensor([lmax, lmax, lmax + 1], dtype=torch.int32, device="cuda")
+    gi, gv, _, st = run_hip(x, offs, lens, K, trace=False)
+    del x
+    torch.cuda.empty_cache()
+    want = {int(p): int(v) for p, v in zip(pos, vals.view(np.uint32))}
+    for r, shift in ((0, 0), (1, 3)):
+        got = {int(i) + shift: int(v) for i, v in zip(gi[r], gv[r].view(np.uint32))}
+        assert got == want, f"row {r}: {len(set(got) ^ set(want))} positions differ"
+    assert np.all(gi[2] == -1) and np.all(np.isneginf(gv[2]))
+    assert st["errors"] == 1, st
+    say("routes", st)
