@@ -265,3 +265,26 @@ def test_concurrent_calls_with_separate_workspaces(topk, seed):
         for w, st, s, o, l, ws, gi, gv, (oi, ov) in calls:
             assert_same_selection(gi.cpu().numpy(), gv.cpu().numpy(), oi, ov,
                                   where=f"{w.name}, concurrent, rep {rep}")
+
+
+@pytest.mark.parametrize("shift", [1, 2, 3])
+def test_mixed_call_misaligned_scores_pointer(topk, shift):
+    """The scores pointer itself 4, 8 or 12 bytes past a 16-byte boundary (a
+    slice of a larger buffer), on top of the rows' own odd offsets."""
+    import torch
+
+    import oracle
+    from tests.gpu_util import assert_same_selection, run_hip
+
+    wl = mixed_workload(20 + shift)
+    big = torch.zeros(wl.scores.size + 4, dtype=torch.float32, device="cuda")
+    big[shift:shift + wl.scores.size] = torch.from_numpy(wl.scores).cuda()
+    s = big[shift:shift + wl.scores.size]
+    assert s.data_ptr() % 16 == 4 * shift
+    o = torch.from_numpy(wl.row_offsets).cuda()
+    l = torch.from_numpy(wl.row_lengths).cuda()
+    say("scores pointer +", 4 * shift, "bytes: rows", wl.n_rows, "K", wl.K)
+    gi, gv, _, st = run_hip(s, o, l, wl.K, topk.policy_for_k(wl.K), trace=False)
+    oi, ov = oracle.topk_ragged(wl.scores, wl.row_offsets, wl.row_lengths, wl.K)
+    assert_same_selection(gi, gv, oi, ov, where=f"scores pointer +{4 * shift} B")
+    assert st["errors"] == 0
