@@ -1216,72 +1216,107 @@ __device__ __forceinline__ void refine(const KArgs a, Smem &sm, int r, bool segm
 
 // ------------------------------------------------------ exact routes ----
 
-__device__ __forceinline__ uint64_t composite(uint32_t key, uint32_t idx) {
-    return ((uint64_t)key << 32) | idx;
-}
-
 // Resolves an exact boundary bin that exceeds the frontier capacity without
-// materialising it: each round re-reads the row and histograms the next digit
-// of the composite key (kappa32, index) among boundary-bin elements that
-// match the digits fixed so far, until the k-th smallest key T is known; a
-// last pass commits every boundary-bin element with key <= T.
+// materialising it; every pass re-reads the row.  The bin is a contiguous
+// range of ascending FP32 keys, [bin_cutoff(t*), bin_cutoff(t* - 1) - 1].
+// Digit rounds narrow a window on the key, largest keys first, until the
+// k-th largest key uT of the bin is known; when more elements hold uT than
+// are still needed, rounds over the row index narrow a window on the index,
+// lowest first (the composite order (kappa32, index)).  A last pass commits
+// every bin element above uT and those at uT with index <= iT.  A pass costs
+// a range test per element; only elements inside the window go further.
 __device__ __forceinline__ void reread_select(const KArgs a, Smem &sm, int r, int64_t off, int64_t L,
                               uint32_t tstar, uint32_t k) {
     const int tid = threadIdx.x;
     const float *scores = a.scores;
-    uint64_t prefix = 0; // chosen digits so far, left-aligned in the 64-bit key
-    int shift_done = 64; // bits of the composite key fixed = 64 - shift_done
-    uint64_t T = ~0ull; // select composite <= T
-    for (int j = 0; j < 6; j++) {
-        const int w = (j % 3 == 2) ? 10 : 11;
-        const int shift = shift_done - w;
+    const int32_t n = (int32_t)L;
+    const uint32_t bhi = tstar == 0u ? 0xFFFFFFFFu : bin_cutoff(tstar - 1u) - 1u;
+    uint32_t wlo = bin_cutoff(tstar), whi = bhi;  // key window
+    uint32_t ilo = 0u, ihi = (uint32_t)(n - 1);   // index window at key uT
+    uint32_t uT = wlo, iT = 0xFFFFFFFFu;
+    bool by_key = wlo != whi;
+    // every round narrows its window to fewer than 2^11 parts of it, so the
+    // key takes at most three rounds and the index three more
+    for (int round = 0; round < 6; round++) {
+        const uint32_t span = by_key ? whi - wlo : ihi - ilo;
+        if (span == 0u) break;                     // one key / one index left
+        const int s = max(0, 21 - (int)__builtin_clz(span)); // span >> s < 2^11
         clear_hist(sm);
         __syncthreads();
-        const uint64_t hi_mask = (shift_done >= 64) ? 0ull : (~0ull << shift_done);
-        stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                                 int32_t hi, bool, int32_t mv) {
+        if (by_key) {
+            stream_row<false>(scores, off, 0, n, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                                     int32_t hi, bool edge, int32_t mv) {
 #pragma unroll
-            for (int m = 0; m < kVec; m++) if (m < mv) {
+                for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
-                for (int c = 0; c < 4; c++) {
-                    const int32_t i = i0[m] + c;
-                    if (!in_window(i, lo, hi)) continue;
-                    if (coarse_bin(x[m][c]) != tstar) continue;
-                    const uint64_t z = composite(~asc_key(fbits(x[m][c])),
-                                                 (uint32_t)i);
-                    if ((z & hi_mask) != prefix) continue;
-                    atomicAdd(&sm.hist[(uint32_t)(z >> shift) & ((1u << w) - 1u)], 1u);
+                    for (int c = 0; c < 4; c++) {
+                        const uint32_t u = asc_key(fbits(x[m][c]));
+                        if (u - wlo <= span && (!edge || in_window(i0[m] + c, lo, hi)))
+                            atomicAdd(&sm.hist[(whi - u) >> s], 1u);
+                    }
                 }
-            }
-        });
+            });
+        } else {
+            stream_row<false>(scores, off, 0, n, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                                     int32_t hi, bool edge, int32_t mv) {
+#pragma unroll
+                for (int m = 0; m < kVec; m++) if (m < mv) {
+#pragma unroll
+                    for (int c = 0; c < 4; c++) {
+                        const uint32_t u = asc_key(fbits(x[m][c]));
+                        const uint32_t di = (uint32_t)(i0[m] + c) - ilo;
+                        if (u == uT && di <= span && (!edge || in_window(i0[m] + c, lo, hi)))
+                            atomicAdd(&sm.hist[di >> s], 1u);
+                    }
+                }
+            });
+        }
         __syncthreads();
         if (tid < 64) wave_find(sm.hist, k, 0, 1, sm.find);
         __syncthreads();
         const Find f = sm.find[0];
-        prefix |= (uint64_t)f.bin << shift;
-        shift_done = shift;
-        const uint32_t need = k - f.below;
         __syncthreads();
-        if (f.eq == need || j == 5) {
-            T = prefix | ((shift == 0) ? 0ull : ((1ull << shift) - 1ull));
-            break;
+        const uint32_t need = k - f.below;
+        if (by_key) {
+            // digit b holds keys whi - u in [b << s, (b + 1) << s)
+            const uint64_t b0 = (uint64_t)f.bin << s, b1 = ((uint64_t)f.bin + 1u) << s;
+            const uint32_t nlo = b1 > (uint64_t)span ? wlo : whi - (uint32_t)(b1 - 1u);
+            whi = whi - (uint32_t)b0;
+            wlo = nlo;
+            uT = wlo;
+            if (f.eq == need) break;               // the whole digit is taken
+            by_key = wlo != whi;                   // else ties at uT: index rounds
+        } else {
+            ilo += f.bin << s;
+            ihi = min(ihi, ilo + ((1u << s) - 1u));
+            iT = ihi;
+            if (f.eq == need) break;
         }
         k = need;
     }
-    // Output pass: every boundary-bin element with composite key <= T.
-    stream_row<false>(scores, off, 0, (int32_t)L, [&](const f4 *x, const int32_t *i0, int32_t lo,
-                                             int32_t hi, bool, int32_t mv) {
+    // Output pass: bin elements with key above uT, and those at uT with index <= iT.
+    const uint32_t tspan = bhi - uT;
+    stream_row<false>(scores, off, 0, n, [&](const f4 *x, const int32_t *i0, int32_t lo,
+                                             int32_t hi, bool edge, int32_t mv) {
 #pragma unroll
         for (int m = 0; m < kVec; m++) if (m < mv) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
+                const uint32_t u = asc_key(fbits(x[m][c]));
                 const int32_t i = i0[m] + c;
-                if (!in_window(i, lo, hi)) continue;
-                if (coarse_bin(x[m][c]) != tstar) continue;
-                const uint32_t key = ~asc_key(fbits(x[m][c]));
-                if (composite(key, (uint32_t)i) > T) continue;
-                const uint32_t op = atomicAdd(&sm.opos, 1u);
-                emit(a, r, op, (uint32_t)i, key);
+                const bool sel = u - uT <= tspan && (u != uT || (uint32_t)i <= iT) &&
+                                 (!edge || in_window(i, lo, hi));
+                const uint64_t em = __ballot(sel);
+                if (em == 0) continue;
+                // one position claim per wave (the output order is free)
+                const int lead = __builtin_ctzll(em);
+                uint32_t op = 0u;
+                if (lane_id() == lead) op = atomicAdd(&sm.opos, (uint32_t)__popcll(em));
+                op = __builtin_amdgcn_readlane(op, lead);
+                if (sel)
+                    emit(a, r, op + __builtin_amdgcn_mbcnt_hi((uint32_t)(em >> 32),
+                                         __builtin_amdgcn_mbcnt_lo((uint32_t)em, 0u)),
+                         (uint32_t)i, ~u);
             }
         }
     });

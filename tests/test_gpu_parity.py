@@ -283,6 +283,76 @@ def test_long_tie_row_uses_index_digits(topk):
     assert st["reread"] >= 1
 
 
+def _reread_rows(rng, L=131072):
+    """Rows whose boundary coarse bin holds more entries than the frontier, so
+    that the re-read path resolves it (K = 2048, 1500 to 1000 clear winners
+    above the bin):
+      keys+ties  distinct keys above a 10000-fold tie inside the bin, then
+                 distinct keys below it: key rounds, then index rounds
+      keys only  8000 distinct keys in one bin: key rounds end the search
+      -inf       1000 finite values and 200 of -1e30 above 129K of -inf
+      +inf bin   +inf, 1e10 and values past the FP16 range in bin 0
+      zero bin   FP32 subnormals and tiny values above 20000 of +0.0, with
+                 20000 of -0.0 (the next bin) and negatives below"""
+    def base(mean=-3.0):
+        return rng.normal(mean, 0.5, L).astype(np.float32)
+
+    def put(x, vals):
+        x[rng.choice(L, len(vals), replace=False)] = np.asarray(vals, np.float32)
+        return x
+
+    rows = {}
+    x = base()
+    # 1500 clear winners; bin of [2.0, 2.0625) (FP16 bin of 32 values at ulp 2^-9)
+    pos = rng.choice(L, 1500 + 300 + 10000 + 2000, replace=False)
+    x[pos[:1500]] = rng.uniform(5.0, 9.0, 1500).astype(np.float32)
+    x[pos[1500:1800]] = rng.uniform(2.0400, 2.0600, 300).astype(np.float32)
+    x[pos[1800:11800]] = np.float32(2.0390625)
+    x[pos[11800:]] = rng.uniform(2.0005, 2.0380, 2000).astype(np.float32)
+    rows["keys+ties"] = x
+    x = base()
+    pos = rng.choice(L, 1500 + 8000, replace=False)
+    x[pos[:1500]] = rng.uniform(5.0, 9.0, 1500).astype(np.float32)
+    x[pos[1500:]] = rng.uniform(2.0005, 2.0600, 8000).astype(np.float32)
+    rows["keys only"] = x
+    x = np.full(L, -np.inf, np.float32)
+    rows["-inf"] = put(put(x, rng.standard_normal(1000)), np.full(200, -1e30))
+    x = base()
+    vals = np.concatenate([np.full(3000, np.inf), np.full(3000, 1e10),
+                           rng.uniform(65600.0, 1e9, 4000)])
+    rows["+inf bin"] = put(x, vals)
+    x = base()
+    pos = rng.choice(L, 1000 + 300 + 20000 + 20000, replace=False)
+    x[pos[:1000]] = rng.uniform(1.0, 3.0, 1000).astype(np.float32)
+    tiny = np.concatenate([np.frombuffer(rng.integers(1, 1 << 23, 150, dtype=np.uint32).tobytes(),
+                                         np.float32), rng.uniform(1e-12, 1e-9, 150)])
+    x[pos[1000:1300]] = tiny.astype(np.float32)
+    x[pos[1300:21300]] = np.float32(0.0)
+    x[pos[21300:]] = np.float32(-0.0)
+    rows["zero bin"] = x
+    return rows
+
+
+@pytest.mark.parametrize("item_table", [False, True], ids=["split-plan", "item-table"])
+def test_reread_windows(topk, item_table):
+    """The re-read path's key and index windows, bit-exact with the oracle in
+    both kernel instances (a call of a few rows, and one of more rows than
+    resident workgroups, run from the item table)."""
+    rng = np.random.default_rng(23)
+    rows = list(_reread_rows(rng).values())
+    if item_table:
+        # 600 rows: the re-read rows among short rows of the direct and exact routes
+        short = [rng.standard_normal(int(n)).astype(np.float32)
+                 for n in rng.integers(100, 6000, 600 - len(rows))]
+        rows = short[:300] + rows + short[300:]
+    lens = np.array([r.size for r in rows], np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    wl = W.Workload("re-read windows", np.concatenate(rows), offs, lens, 2048, "")
+    gt, st = parity(topk, wl, where=f"re-read windows, item table {item_table}")
+    say("routes", st)
+    assert st["reread"] >= 5
+
+
 def test_zero_rows_noop(topk):
     import torch
 
