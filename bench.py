@@ -334,7 +334,8 @@ def time_calls(wl, policy, steps, warmup, rotate=True, calls_per_graph=0, rounds
     return out
 
 
-ABLATIONS = ("margin", "stride", "rescue", "crossover", "k", "recal", "recal-crossover", "batch")
+ABLATIONS = ("margin", "stride", "rescue", "crossover", "k", "recal", "recal-crossover", "batch",
+             "ties")
 
 
 def ablation(name, wl, steps, warmup):
@@ -393,6 +394,10 @@ def ablation(name, wl, steps, warmup):
     elif name == "batch":     # decode rows, more of them: where the latency chain amortises
         for n in (16, 32, 64, 128, 256, 512, 1024):
             variants.append((f"rows={n}", W.decode(n_rows=n), None))
+    elif name == "ties":      # decode-shaped rows with heavy ties (exact route, re-read)
+        variants = [("decode rows", W.decode(), None),
+                    ("clustered 256-value codebook per row", W.decode_ties("clustered"), None),
+                    ("8000 ties above the K-th score", W.decode_ties("block"), None)]
     elif name == "recal-crossover":  # per-K policy: sampled against exact on short rows
         for K in (256, 512, 1024, 2048, 4096):
             kp = topk.policy_for_k(K).as_dict()

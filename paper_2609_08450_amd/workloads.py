@@ -196,6 +196,32 @@ def adversarial(seed: int = BASE_SEED + 5, n_rows: int = 1024, K: int = 2048,
                     f"N({onstride_mean},{onstride_sd}), 30% -inf), K={K}")
 
 
+def decode_ties(kind: str, seed: int = BASE_SEED + 7, K: int = 2048) -> Workload:
+    """Decode-shaped rows (the decode batch's lengths) with heavy ties:
+    kind "clustered": each row drawn from its own codebook, the lowest 256 of
+    4096 N(0,1) draws (so about a dozen codebook values share a coarse bin,
+    and the boundary bin of the longer rows holds more than the frontier);
+    kind "block": the decode mixture rows with 8000 random positions set to
+    one value just above the row's K-th largest score."""
+    base = decode()
+    g = np.random.default_rng(seed)
+    rows = []
+    for r in range(base.n_rows):
+        L = int(base.row_lengths[r])
+        if kind == "clustered":
+            book = np.unique(g.standard_normal(4096, dtype=np.float32))[:256]
+            x = book[g.integers(0, book.size, L)]
+        elif kind == "block":
+            x = base.row(r).copy()
+            x[g.choice(L, 8000, replace=False)] = np.partition(x, L - K)[L - K] + np.float32(0.01)
+        else:
+            raise ValueError(kind)
+        rows.append(x.astype(np.float32, copy=False))
+    buf, offs, ls = _pack(rows)
+    return Workload(f"decode ties ({kind})", buf, offs, ls, K,
+                    f"decode lengths, heavy ties ({kind}), K={K}")
+
+
 def adversarial_recovery(seed: int = BASE_SEED + 6, n_rows: int = 256) -> Workload:
     """Variant of the edge mix whose strided rows carry N(3, 0.5) on the view
     residue: the view then sees only high values, the proposal underfills and

@@ -353,6 +353,16 @@ def test_reread_windows(topk, item_table):
     assert st["reread"] >= 5
 
 
+@pytest.mark.parametrize("kind", ["clustered", "block"])
+def test_decode_ties(topk, kind):
+    """Decode-shaped batches with heavy ties (the rows of bench.py's ties
+    ablation): every row's selection and trace, re-read rows included."""
+    wl = W.decode_ties(kind)
+    gt, st = parity(topk, wl, where=f"decode ties {kind}")
+    say("routes", st)
+    assert st["reread"] >= (64 if kind == "block" else 1)
+
+
 def test_zero_rows_noop(topk):
     import torch
 

@@ -307,6 +307,23 @@ def test_route_model_adversarial_rows():
     assert np.any(strided[:, 0] == oracle.ROUTE_EXACT_UNDERFILL)
 
 
+@pytest.mark.parametrize("kind", ["clustered", "block"])
+def test_route_model_tie_rows(kind):
+    """Decode-shaped rows with heavy ties: a boundary bin over the frontier
+    is resolved by re-reading (every "block" row, the longer "clustered"
+    rows), and the exact route's invariants hold on a sample of rows."""
+    wl = W.decode_ties(kind)
+    _, _, tr = oracle.route_model(wl.scores, wl.row_offsets, wl.row_lengths, wl.K,
+                                  oracle.default_policy())
+    reread = (tr[:, 0] & oracle.ROUTE_REREAD_FLAG) != 0
+    if kind == "block":
+        assert reread.all()
+    else:
+        assert 0 < reread.sum() < wl.n_rows
+        assert wl.row_lengths[reread].min() > wl.row_lengths[~reread].min()
+    _route_checks(wl, wl.K, oracle.default_policy(), rows=range(0, 64, 8))
+
+
 @pytest.mark.parametrize("s,cap,lmin", [(64, 8192, 0), (128, 600, 0), (256, 8192, 4096), (2, 50, 0)])
 def test_route_model_policies(s, cap, lmin):
     rng = np.random.default_rng(s + cap)
