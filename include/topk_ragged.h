@@ -60,8 +60,8 @@ extern "C" {
  * route. */
 #define TOPK_K_MAX 16384
 /* Longest row, in elements: the kernels address a row's 16-byte vectors with
- * 32-bit byte offsets from its base. */
-#define TOPK_L_MAX 0x3FFFFFFB
+ * 32-bit byte offsets from the 128-byte line that holds its first element. */
+#define TOPK_L_MAX 0x3FFFFFDF
 /* Frontier capacity of one workgroup, in (index, key) pairs. */
 #define TOPK_FRONTIER_CAP 6144
 /* Words per row written by topk_ragged_ex when row_trace is not NULL. */

@@ -447,8 +447,9 @@ struct NeverStop {
 };
 
 // A row range as 16-byte vectors: [beg, end) of the row at element offset
-// off, covered by nvec vectors from vbase (aligned down to 16 bytes; ibase is
-// the row index of vbase's first element), in nch chunks of kChunkVecs.
+// off, covered by nvec vectors from vbase (the start of the 128-byte line
+// holding element beg; ibase is the row index of vbase's first element), in
+// nch chunks of kChunkVecs.
 struct RowVecs {
     const char *vbase;
     int32_t ibase, nvec, nch;
@@ -458,7 +459,11 @@ __device__ __forceinline__ RowVecs row_vecs(const float *scores, int64_t off, in
                                             int32_t end) {
     const uintptr_t sp = reinterpret_cast<uintptr_t>(scores);
     const int64_t sh = (int64_t)((sp & 15) >> 2);
-    const int64_t v0 = (off + beg + sh) >> 2;
+    // The first vector is that of the 128-byte line holding element beg, so
+    // each wave's 64 vectors of a chunk cover eight whole lines, not parts
+    // of nine (the elements before beg are masked by the window test; the
+    // line holds a valid element, so it lies in mapped memory).
+    const int64_t v0 = ((off + beg + sh) >> 2) & ~(int64_t)7;
     RowVecs g;
     g.nvec = (int32_t)(((off + end + sh + 3) >> 2) - v0);
     g.vbase = reinterpret_cast<const char *>(sp & ~(uintptr_t)15) + v0 * 16;

@@ -819,9 +819,11 @@ def test_read_ceiling_reads_every_score(topk, cfg):
 
 
 def test_rows_at_the_length_limit(topk):
-    """Rows of exactly TOPK_L_MAX elements (2^30 - 5), at an aligned offset and
-    at the worst misalignment (3 elements), whose Top-K is known by
-    construction: K distinct positive values planted among negative ones.
+    """Rows of exactly TOPK_L_MAX elements (2^30 - 33), at an aligned offset and
+    at the worst misalignment (31 elements: the last of a 128-byte line, so
+    the streamed range starts 31 elements before the row), whose Top-K is
+    known by construction: K distinct positive values planted among negative
+    ones.
     Both return exactly the planted (index, value) set.  A row one element
     longer is rejected on the device: -1 / -inf and one error count."""
     import re
@@ -832,19 +834,19 @@ def test_rows_at_the_length_limit(topk):
     lmax = int(re.search(r"#define TOPK_L_MAX (0x[0-9A-Fa-f]+)", text).group(1), 16)
     K = 2048
     say("rows of", lmax, "elements")
-    x = torch.rand(lmax + 4, device="cuda")
+    x = torch.rand(lmax + 32, device="cuda")
     x.add_(1.0).neg_()                            # every value in (-2, -1]
     rng = np.random.default_rng(71)
-    pos = np.sort(rng.choice(np.arange(3, lmax, dtype=np.int64), K, replace=False))
+    pos = np.sort(rng.choice(np.arange(31, lmax, dtype=np.int64), K, replace=False))
     vals = (1.0 + rng.permutation(K) / 4096.0).astype(np.float32)
     x[torch.from_numpy(pos).cuda()] = torch.from_numpy(vals).cuda()
-    offs = torch.tensor([0, 3, 0], dtype=torch.int64, device="cuda")
+    offs = torch.tensor([0, 31, 0], dtype=torch.int64, device="cuda")
     lens = torch.tensor([lmax, lmax, lmax + 1], dtype=torch.int32, device="cuda")
     gi, gv, _, st = run_hip(x, offs, lens, K, trace=False)
     del x
     torch.cuda.empty_cache()
     want = {int(p): int(v) for p, v in zip(pos, vals.view(np.uint32))}
-    for r, shift in ((0, 0), (1, 3)):
+    for r, shift in ((0, 0), (1, 31)):
         got = {int(i) + shift: int(v) for i, v in zip(gi[r], gv[r].view(np.uint32))}
         assert got == want, f"row {r}: {len(set(got) ^ set(want))} positions differ"
     assert np.all(gi[2] == -1) and np.all(np.isneginf(gv[2]))

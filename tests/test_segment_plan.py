@@ -75,11 +75,12 @@ def _header_define(name):
 
 
 def _max_vector_byte_offset(off, beg, end, sh):
-    """The row streaming's largest 16-byte vector offset from its aligned
-    base: nvec = ceil((off + end + sh) / 4) - floor((off + beg + sh) / 4)
-    vectors, the last at byte (nvec - 1) * 16 (sh = the buffer's misalignment
-    in elements, 0..3)."""
-    v0 = (off + beg + sh) >> 2
+    """The row streaming's largest 16-byte vector offset from its base, the
+    start of the 128-byte line holding element beg: the first vector is
+    floor((off + beg + sh) / 4) rounded down to a multiple of 8, nvec =
+    ceil((off + end + sh) / 4) - that, the last at byte (nvec - 1) * 16 (sh =
+    the buffer's misalignment in elements, 0..3)."""
+    v0 = ((off + beg + sh) >> 2) & ~7
     nvec = ((off + end + sh + 3) >> 2) - v0
     return (nvec - 1) * 16
 
@@ -91,8 +92,8 @@ def test_longest_row_keeps_32_bit_vector_offsets():
     lmax = _header_define("TOPK_L_MAX")
     worst = 0
     for sh in range(4):
-        for off in range(8):
+        for off in range(32):
             worst = max(worst, _max_vector_byte_offset(off, 0, lmax, sh))
     assert worst < 2**32
-    wraps = max(_max_vector_byte_offset(off, 0, lmax + 4, sh) for sh in range(4) for off in range(8))
+    wraps = max(_max_vector_byte_offset(off, 0, lmax + 4, sh) for sh in range(4) for off in range(32))
     assert wraps >= 2**32
